@@ -1,0 +1,22 @@
+"""fp64 CPU oracle of the SAF3R hot path (test infrastructure only).
+
+Only the tests, the smoke check and the benchmark's CPU-baseline leg import
+this package; the product path never does.
+"""
+from .saf3r_oracle import *  # noqa: F401,F403
+from .saf3r_oracle import (  # noqa: F401
+    attend_block,
+    attend_head,
+    block_range,
+    block_scores,
+    dense_attention,
+    frame_local_row,
+    kept_fraction,
+    nmse,
+    num_blocks,
+    pool_blocks,
+    run_layer,
+    select_head,
+    to_f64,
+    topk_row,
+)

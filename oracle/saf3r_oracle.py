@@ -1,0 +1,239 @@
+"""Plain fp64 CPU oracle of the SAF3R online hot path.
+
+TEST INFRASTRUCTURE ONLY. Only the tests, the smoke check and the benchmark's
+CPU-baseline leg may import this module. The product path (the HIP library and
+its Python binding) never calls it and must fail loudly when the HIP library
+is missing.
+
+It follows the paper (SAF3R: Dynamic Sparse Attention for Feed-Forward 3D
+Reconstruction Transformers) step by step, in float64, with no blocking,
+fusion or reordering beyond what the definitions state:
+
+1. Pooling (Sec. 4.3, Query-Probe Top-K): the probe of a set of queries is
+   their mean. Read per query block of ``block`` tokens (and likewise per key
+   block) over the tokens the block actually holds.
+2. Scores (Sec. 4.3): by linearity of the inner product, the mean of the
+   pre-softmax scores ``S = Q K^T / sqrt(D)`` over a (query block, key block)
+   tile equals the scaled inner product of the two pooled vectors.
+3. Selection per head class (Sec. 4.1 kernels; the class comes from the
+   offline profile of Sec. 4.2): DENSE keeps every key block, FRAME_LOCAL (the
+   static kernel) keeps the key blocks that share a frame with the query
+   block, TOPK (the query-probe kernel) keeps the ``k`` best-scoring key blocks
+   with ties broken towards the lower block index.
+4. Attention restricted to the kept keys (Sec. 4.1, Query-Probe Top-K kernel):
+   softmax over the union of the kept key blocks' tokens, renormalised over
+   that set, times V.
+5. NMSE (Sec. 4.2, Eq. 1) between full and sparse outputs, as a quality
+   report.
+
+Pins (checked by the CPU tests, not by this module): pooling+scores against
+the brute-force tile mean of S; Top-K against brute force over all k-subsets;
+frame-local lists against a hand-worked example and special cases; attention
+against a library softmax attention with an explicit token mask; NMSE
+against closed forms. Every function here is pinned.
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+DENSE = 0
+FRAME_LOCAL = 1
+TOPK = 2
+
+
+# --------------------------------------------------------------------------
+# inputs
+
+
+def to_f64(x: np.ndarray, dtype: str) -> np.ndarray:
+    """Exact widening to float64 of fp32 values or of bf16 bit patterns."""
+    if dtype == "bf16":
+        bits = np.ascontiguousarray(x, dtype=np.uint16).astype(np.uint32) << 16
+        return bits.view(np.float32).astype(np.float64)
+    if dtype == "f32":
+        return np.asarray(x, dtype=np.float32).astype(np.float64)
+    raise ValueError(dtype)
+
+
+def num_blocks(n: int, block: int) -> int:
+    return (n + block - 1) // block
+
+
+def block_range(b: int, n: int, block: int) -> range:
+    """Tokens held by block ``b``; the last block may hold fewer than ``block``."""
+    return range(b * block, min((b + 1) * block, n))
+
+
+# --------------------------------------------------------------------------
+# 1-2. pooling and block scores (Sec. 4.3)
+
+
+def pool_blocks(x: np.ndarray, block: int) -> np.ndarray:
+    """Mean of the rows of each block: ``x [N, D]`` -> ``[nb, D]``.
+
+    The probe of Sec. 4.3 is the mean of the queries; per block, the mean is
+    over the tokens the block holds (a partial last block divides by its own
+    count)."""
+    n, d = x.shape
+    nb = num_blocks(n, block)
+    out = np.empty((nb, d), np.float64)
+    for b in range(nb):
+        r = block_range(b, n, block)
+        out[b] = x[r.start:r.stop].sum(axis=0) / len(r)
+    return out
+
+
+def block_scores(q_pooled: np.ndarray, k_pooled: np.ndarray) -> np.ndarray:
+    """``s[i, j] = qbar_i . kbar_j / sqrt(D)``: the mean of S over tile (i, j)."""
+    d = q_pooled.shape[1]
+    return (q_pooled @ k_pooled.T) / math.sqrt(d)
+
+
+# --------------------------------------------------------------------------
+# 3. selection (Sec. 4.1 kernels, Sec. 4.3 Top-K)
+
+
+def frames_of_block(b: int, n: int, tokens_per_frame: int, block: int) -> set:
+    return {t // tokens_per_frame for t in block_range(b, n, block)}
+
+
+def frame_local_row(i: int, n: int, tokens_per_frame: int, block: int) -> np.ndarray:
+    """Key blocks sharing at least one frame with query block ``i`` (static
+    kernel, block granularity)."""
+    fi = frames_of_block(i, n, tokens_per_frame, block)
+    nb = num_blocks(n, block)
+    keep = [j for j in range(nb) if fi & frames_of_block(j, n, tokens_per_frame, block)]
+    return np.asarray(keep, np.int64)
+
+
+def topk_row(scores_row: np.ndarray, k: int):
+    """The ``k`` best key blocks of one query block.
+
+    Order: score descending, then block index ascending (stable), first ``k``
+    taken. Returns (ascending indices, margin) where the margin is the gap
+    between the k-th and (k+1)-th ranked scores (+inf when every block is
+    kept)."""
+    nb = scores_row.shape[0]
+    order = np.lexsort((np.arange(nb), -scores_row))
+    chosen = np.sort(order[:k])
+    margin = math.inf if k >= nb else float(scores_row[order[k - 1]] - scores_row[order[k]])
+    return chosen.astype(np.int64), margin
+
+
+def select_head(pattern: int, topk: int, q_head: np.ndarray, k_head: np.ndarray,
+                tokens_per_frame: int, block: int):
+    """Kept key blocks of every query block of one head.
+
+    Returns (lists, margins, scores): ``lists[i]`` ascending int64, ``margins``
+    the Top-K margins (+inf for the other classes), ``scores`` the block score
+    matrix for Top-K heads (None otherwise)."""
+    n = q_head.shape[0]
+    nb = num_blocks(n, block)
+    margins = np.full(nb, math.inf)
+    if pattern == DENSE:
+        return [np.arange(nb, dtype=np.int64) for _ in range(nb)], margins, None
+    if pattern == FRAME_LOCAL:
+        return [frame_local_row(i, n, tokens_per_frame, block) for i in range(nb)], margins, None
+    if pattern == TOPK:
+        if not 1 <= topk <= nb:
+            raise ValueError("topk out of range")
+        s = block_scores(pool_blocks(q_head, block), pool_blocks(k_head, block))
+        lists = []
+        for i in range(nb):
+            sel, margins[i] = topk_row(s[i], topk)
+            lists.append(sel)
+        return lists, margins, s
+    raise ValueError(f"unknown pattern {pattern}")
+
+
+# --------------------------------------------------------------------------
+# 4. attention over the kept keys (Sec. 4.1)
+
+
+def attend_block(q_head: np.ndarray, k_head: np.ndarray, v_head: np.ndarray, i: int,
+                 kept: np.ndarray, block: int):
+    """Output rows and log-sum-exp of query block ``i`` over the kept key blocks.
+
+    Softmax of ``q . k / sqrt(D)`` over the union of the kept blocks' tokens,
+    renormalised over that set, applied to V."""
+    n, d = q_head.shape
+    rows = block_range(i, n, block)
+    if len(kept) == 0:
+        raise ValueError("a query block must keep at least one key block")
+    spans = [block_range(int(j), n, block) for j in kept]
+    keys = np.concatenate([np.arange(r.start, r.stop) for r in spans])
+    z =(q_head[rows.start:rows.stop] @ k_head[keys].T) / math.sqrt(d)
+    zmax = z.max(axis=1, keepdims=True)
+    e = np.exp(z - zmax)
+    denom = e.sum(axis=1, keepdims=True)
+    out = (e / denom) @ v_head[keys]
+    lse = (zmax + np.log(denom))[:, 0]
+    return out, lse
+
+
+def attend_head(q_head, k_head, v_head, lists, block: int):
+    n, d = q_head.shape
+    out = np.empty((n, d), np.float64)
+    lse = np.empty(n, np.float64)
+    for i, kept in enumerate(lists):
+        r = block_range(i, n, block)
+        out[r.start:r.stop], lse[r.start:r.stop] = attend_block(q_head, k_head, v_head, i, kept, block)
+    return out, lse
+
+
+def dense_attention(q_head, k_head, v_head):
+    """Full softmax attention of one head (the paper's "Full" reference)."""
+    d = q_head.shape[1]
+    z = (q_head @ k_head.T) / math.sqrt(d)
+    zmax = z.max(axis=1, keepdims=True)
+    e = np.exp(z - zmax)
+    denom = e.sum(axis=1, keepdims=True)
+    return (e / denom) @ v_head, (zmax + np.log(denom))[:, 0]
+
+
+# --------------------------------------------------------------------------
+# 5. quality report (Sec. 4.2, Eq. 1)
+
+
+def nmse(o_full: np.ndarray, o_sparse: np.ndarray) -> float:
+    """``||O_full - O_sparse||^2 / ||O_full||^2`` for one head and one input."""
+    num = float(np.sum((o_full - o_sparse) ** 2))
+    den = float(np.sum(o_full ** 2))
+    return num / den
+
+
+# --------------------------------------------------------------------------
+# whole layer
+
+
+def kept_fraction(lists_per_head, nb: int) -> float:
+    """Fraction of (query block, key block) pairs kept over all heads."""
+    kept = sum(len(x) for lists in lists_per_head for x in lists)
+    return kept / (len(lists_per_head) * nb * nb)
+
+
+def run_layer(q, k, v, table, tokens_per_frame: int, dtype: str, block: int = 64,
+              heads=None, with_attention: bool = True):
+    """The whole hot path for one layer.
+
+    ``q, k, v``: ``[H, N, D]`` fp32 arrays or bf16 bit patterns; ``table``:
+    per-head ``(pattern, topk)``. Returns a dict with per-head lists, margins,
+    pooled vectors (Top-K heads), scores, outputs and log-sum-exps (float64)."""
+    H = q.shape[0]
+    heads = range(H) if heads is None else heads
+    res = {"lists": {}, "margins": {}, "scores": {}, "q_pooled": {}, "k_pooled": {},
+           "out": {}, "lse": {}}
+    for h in heads:
+        pattern, topk = table[h]
+        qh, kh = to_f64(q[h], dtype), to_f64(k[h], dtype)
+        lists, margins, s = select_head(pattern, topk, qh, kh, tokens_per_frame, block)
+        res["lists"][h], res["margins"][h], res["scores"][h] = lists, margins, s
+        if pattern == TOPK:
+            res["q_pooled"][h] = pool_blocks(qh, block)
+            res["k_pooled"][h] = pool_blocks(kh, block)
+        if with_attention:
+            vh = to_f64(v[h], dtype)
+            res["out"][h], res["lse"][h] = attend_head(qh, kh, vh, lists, block)
+    return res
