@@ -1,0 +1,152 @@
+/*
+ * saf3r.h -- C ABI of the SAF3R block-sparse global-attention hot path for
+ * AMD Instinct MI355X (gfx950).
+ *
+ * SAF3R (Dynamic Sparse Attention for Feed-Forward 3D Reconstruction
+ * Transformers) gives every attention head of a cross-view global-attention
+ * layer a sparse pattern class chosen offline (Sec. 4.2) and, for dynamic
+ * heads, picks the kept keys online from a cheap probe (Sec. 4.3). This
+ * library runs that online stage at block granularity in three calls:
+ *
+ *   saf3r_estimate_blocks   pooled (mean) Q and K per 64-token block
+ *   saf3r_select_blocks     kept key blocks per query block, per head class
+ *   saf3r_sparse_attention  softmax attention over the kept blocks only
+ *
+ * Tensor conventions (all calls):
+ *   - Q, K, V, O are device arrays [heads, N, 64], row-major, N = frames *
+ *     tokens_per_frame (tokens of frame f are [f*T, (f+1)*T)); element type
+ *     is bf16 (SAF3R_BF16) or fp32 (SAF3R_F32), the same for all four.
+ *   - Blocks are 64 tokens: block b holds tokens [64b, min(64b+64, N)); the
+ *     last block may be partial. nb = ceil(N / 64).
+ *   - Every device pointer is owned by the caller, must be valid for the
+ *     sizes stated, and must not alias another argument. The library
+ *     allocates nothing and keeps no state between calls; calls on different
+ *     streams may run concurrently when their outputs do not overlap.
+ *   - `problem` and `table` are host pointers read during the call only.
+ *   - `stream` is a hipStream_t (NULL = the default stream). Work is enqueued
+ *     asynchronously; the call returns after the launches.
+ *   - Every argument is validated on the host before anything is launched; a
+ *     call that returns an error has enqueued nothing. SAF3R_ERR_HIP reports
+ *     a launch error from the HIP runtime.
+ */
+#ifndef SAF3R_H
+#define SAF3R_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  SAF3R_OK = 0,
+  SAF3R_ERR_INVALID_ARGUMENT = -1, /* null pointer, non-positive size, bad dtype */
+  SAF3R_ERR_UNSUPPORTED = -2,      /* head_dim or block other than 64, sizes beyond the limits */
+  SAF3R_ERR_CAPACITY = -3,         /* cap smaller than saf3r_index_capacity() */
+  SAF3R_ERR_HIP = -4,              /* the HIP runtime reported an error on launch */
+  SAF3R_ERR_BAD_TABLE = -5         /* unknown pattern class, or Top-K budget outside [1, nb] */
+} saf3r_status;
+
+typedef enum { SAF3R_F32 = 0, SAF3R_BF16 = 1 } saf3r_dtype;
+
+/* Head pattern classes (Sec. 4.1 kernels; assignment from the offline
+ * profile of Sec. 4.2):
+ *   SAF3R_DENSE        full attention ("Full" in the ablations);
+ *   SAF3R_FRAME_LOCAL  static kernel: a query block keeps every key block
+ *                      that shares at least one frame with it (block
+ *                      granularity, so a block straddling two frames keeps
+ *                      the key blocks of both);
+ *   SAF3R_TOPK         query-probe Top-K kernel (Sec. 4.3) at block level:
+ *                      keep the topk_blocks key blocks j with the largest
+ *                      score qbar_i . kbar_j / sqrt(64), ties to the lower j.
+ */
+typedef enum { SAF3R_DENSE = 0, SAF3R_FRAME_LOCAL = 1, SAF3R_TOPK = 2 } saf3r_pattern;
+
+typedef struct {
+  int32_t pattern;     /* saf3r_pattern */
+  int32_t topk_blocks; /* SAF3R_TOPK: key blocks kept per query block, in [1, nb]; ignored otherwise */
+} saf3r_head_cfg;      /* host array [heads] */
+
+typedef struct {
+  int32_t heads;            /* 1 .. 256 */
+  int32_t frames;           /* >= 1 */
+  int32_t tokens_per_frame; /* >= 1; N = frames * tokens_per_frame, 1 .. 1048576 */
+  int32_t head_dim;         /* must be 64 */
+  int32_t block;            /* must be 64 */
+  int32_t dtype;            /* saf3r_dtype */
+} saf3r_problem;
+
+/* Number of 64-token blocks, ceil(N / 64), or a negative saf3r_status. */
+int32_t saf3r_num_blocks(const saf3r_problem* problem);
+
+/* Smallest `cap` accepted by saf3r_select_blocks / saf3r_sparse_attention:
+ * the longest kept-block list of any FRAME_LOCAL or TOPK head (at least 1),
+ * or a negative saf3r_status. DENSE heads need no list. */
+int32_t saf3r_index_capacity(const saf3r_problem* problem, const saf3r_head_cfg* table);
+
+/* Block pooling (Sec. 4.3: the probe of a set of queries is their mean).
+ * For every TOPK head h and block b:
+ *   q_pooled[h][b][:] = mean of Q[h][t][:] over the tokens t of block b
+ *   k_pooled[h][b][:] = mean of K[h][t][:] likewise
+ * in float64 (a partial last block is divided by its own token count).
+ *   q, k               device, [heads, N, 64] of problem->dtype
+ *   q_pooled, k_pooled device, float64 [heads, nb, 64]; rows of non-TOPK
+ *                      heads are left untouched
+ * Returns SAF3R_OK, or an error with nothing enqueued. */
+saf3r_status saf3r_estimate_blocks(const saf3r_problem* problem, const saf3r_head_cfg* table,
+                                   const void* q, const void* k,
+                                   double* q_pooled, double* k_pooled, void* stream);
+
+/* Kept key blocks per query block (Sec. 4.1 static and query-probe Top-K
+ * kernels; block scores are the exact tile means of Q K^T / sqrt(64),
+ * Sec. 4.3). For head h and query block i:
+ *   DENSE:        block_cnt[h][i] = nb; block_idx[h][i][:] left untouched
+ *                 (attention treats the head as dense);
+ *   FRAME_LOCAL:  the contiguous range of key blocks sharing a frame with i;
+ *   TOPK:         the topk_blocks highest scores s[i][j] = qbar_i . kbar_j / 8
+ *                 (computed in float64), ties to the lower j.
+ * Lists are written ascending, padded with -1 up to cap.
+ *   q_pooled, k_pooled device float64 [heads, nb, 64] from saf3r_estimate_blocks
+ *                      (read for TOPK heads only)
+ *   block_idx          device int32 [heads, nb, cap]
+ *   block_cnt          device int32 [heads, nb]
+ *   cap                >= saf3r_index_capacity(problem, table)
+ *   scores_or_null     NULL, or device float64 [heads, nb, nb]: the full score
+ *                      matrix of every TOPK head (other heads untouched)
+ * Returns SAF3R_OK, or an error with nothing enqueued. */
+saf3r_status saf3r_select_blocks(const saf3r_problem* problem, const saf3r_head_cfg* table,
+                                 const double* q_pooled, const double* k_pooled,
+                                 int32_t* block_idx, int32_t* block_cnt, int32_t cap,
+                                 double* scores_or_null, void* stream);
+
+/* Attention restricted to the kept key blocks (Sec. 4.1: compute only the
+ * scores between the queries and the selected keys, softmax renormalised
+ * over them). For a query token t of block i of head h, with U the tokens of
+ * the blocks listed for (h, i) (all blocks for a DENSE head):
+ *   z_u    = q_t . k_u / 8,  u in U
+ *   out[t] = sum_u softmax(z)_u v_u
+ *   lse[t] = log(sum_u exp(z_u))            (natural log)
+ * bf16 inputs: Q K^T and P V on bf16 matrix cores with fp32 accumulation, the
+ * softmax in fp32, P rounded to bf16 for P V, out rounded to bf16. fp32
+ * inputs: everything in fp32.
+ *   q, k, v      device [heads, N, 64] of problem->dtype
+ *   block_idx, block_cnt, cap   as written by saf3r_select_blocks; entries of
+ *                DENSE heads are not read. A list that is not ascending,
+ *                repeats a block or holds indices outside [0, nb) gives
+ *                unspecified output values but no out-of-bounds access.
+ *   out          device [heads, N, 64] of problem->dtype
+ *   lse_or_null  NULL, or device float32 [heads, N]
+ * Returns SAF3R_OK, or an error with nothing enqueued. */
+saf3r_status saf3r_sparse_attention(const saf3r_problem* problem, const saf3r_head_cfg* table,
+                                    const void* q, const void* k, const void* v,
+                                    const int32_t* block_idx, const int32_t* block_cnt, int32_t cap,
+                                    void* out, float* lse_or_null, void* stream);
+
+/* Static description of a status code (never NULL). */
+const char* saf3r_status_string(int32_t status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SAF3R_H */

@@ -101,11 +101,12 @@ def frames_of_block(b: int, n: int, tokens_per_frame: int, block: int) -> set:
 
 def frame_local_row(i: int, n: int, tokens_per_frame: int, block: int) -> np.ndarray:
     """Key blocks sharing at least one frame with query block ``i`` (static
-    kernel, block granularity)."""
-    fi = frames_of_block(i, n, tokens_per_frame, block)
-    nb = num_blocks(n, block)
-    keep = [j for j in range(nb) if fi & frames_of_block(j, n, tokens_per_frame, block)]
-    return np.asarray(keep, np.int64)
+    kernel, block granularity): the blocks that hold a token whose frame is
+    one of the frames of block ``i``."""
+    fi = np.array(sorted(frames_of_block(i, n, tokens_per_frame, block)))
+    token_frame = np.arange(n) // tokens_per_frame
+    token_block = np.arange(n) // block
+    return np.unique(token_block[np.isin(token_frame, fi)]).astype(np.int64)
 
 
 def topk_row(scores_row: np.ndarray, k: int):

@@ -1,0 +1,21 @@
+"""SAF3R block-sparse global attention for AMD Instinct MI355X (gfx950).
+
+The compute path is the HIP library ``libsaf3r.so`` (C ABI in
+``include/saf3r.h``); ``binding`` marshals torch device tensors into it.
+"""
+from . import binding  # noqa: F401
+from .binding import (  # noqa: F401
+    BF16,
+    DENSE,
+    F32,
+    FRAME_LOCAL,
+    TOPK,
+    Saf3rError,
+    estimate_blocks,
+    index_capacity,
+    load,
+    num_blocks,
+    run_layer,
+    select_blocks,
+    sparse_attention,
+)

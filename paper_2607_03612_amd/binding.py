@@ -1,0 +1,218 @@
+"""Python binding of libsaf3r.so (ctypes): argument marshalling only.
+
+Every computation runs in the HIP library; PyTorch only provides device
+memory and the current HIP stream. Names mirror the C ABI without the
+``saf3r_`` prefix. If the library has not been built, ``load()`` raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libsaf3r.so")
+
+F32, BF16 = 0, 1
+DENSE, FRAME_LOCAL, TOPK = 0, 1, 2
+HEAD_DIM = 64
+BLOCK = 64
+
+EXPORTS = (
+    "saf3r_num_blocks",
+    "saf3r_index_capacity",
+    "saf3r_estimate_blocks",
+    "saf3r_select_blocks",
+    "saf3r_sparse_attention",
+    "saf3r_status_string",
+)
+
+
+class Problem(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in
+                ("heads", "frames", "tokens_per_frame", "head_dim", "block", "dtype")]
+
+
+class HeadCfg(ctypes.Structure):
+    _fields_ = [("pattern", ctypes.c_int32), ("topk_blocks", ctypes.c_int32)]
+
+
+class Saf3rError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        msg = _lib().saf3r_status_string(status).decode() if _LIB else str(status)
+        super().__init__(f"{where}: status {status} ({msg})")
+
+
+_LIB = None
+
+
+def _declare(lib):
+    P, C, V, I32 = ctypes.POINTER(Problem), ctypes.POINTER(HeadCfg), ctypes.c_void_p, ctypes.c_int32
+    lib.saf3r_num_blocks.argtypes = [P]
+    lib.saf3r_num_blocks.restype = I32
+    lib.saf3r_index_capacity.argtypes = [P, C]
+    lib.saf3r_index_capacity.restype = I32
+    lib.saf3r_estimate_blocks.argtypes = [P, C, V, V, V, V, V]
+    lib.saf3r_estimate_blocks.restype = I32
+    lib.saf3r_select_blocks.argtypes = [P, C, V, V, V, V, I32, V, V]
+    lib.saf3r_select_blocks.restype = I32
+    lib.saf3r_sparse_attention.argtypes = [P, C, V, V, V, V, V, I32, V, V, V]
+    lib.saf3r_sparse_attention.restype = I32
+    lib.saf3r_status_string.argtypes = [I32]
+    lib.saf3r_status_string.restype = ctypes.c_char_p
+
+
+def load(path: str = LIB_PATH):
+    """Load the HIP library (raises if it has not been built)."""
+    global _LIB
+    if _LIB is None:
+        if not os.path.exists(path):
+            raise RuntimeError(
+                f"{path} is missing: build it with `python -m paper_2607_03612_amd.build`")
+        lib = ctypes.CDLL(path)
+        _declare(lib)
+        _LIB = lib
+    return _LIB
+
+
+def _lib():
+    return load()
+
+
+# ------------------------------------------------------------ marshalling
+
+
+def problem(heads: int, frames: int, tokens_per_frame: int, dtype: int) -> Problem:
+    return Problem(heads, frames, tokens_per_frame, HEAD_DIM, BLOCK, dtype)
+
+
+def head_table(table) -> ctypes.Array:
+    arr = (HeadCfg * len(table))()
+    for h, (pattern, topk) in enumerate(table):
+        arr[h] = HeadCfg(int(pattern), int(topk))
+    return arr
+
+
+def _torch_dtype_code(t) -> int:
+    import torch
+
+    if t.dtype == torch.bfloat16:
+        return BF16
+    if t.dtype == torch.float32:
+        return F32
+    raise ValueError(f"unsupported dtype {t.dtype}")
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    import torch
+
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _check(status: int, where: str):
+    if status != 0:
+        raise Saf3rError(status, where)
+
+
+def _check_qkv(*ts):
+    t0 = ts[0]
+    for t in ts:
+        if not (t.is_cuda and t.is_contiguous() and t.dim() == 3 and t.shape[2] == HEAD_DIM):
+            raise ValueError("expected contiguous device tensors of shape [heads, N, 64]")
+        if t.shape != t0.shape or t.dtype != t0.dtype or t.device != t0.device:
+            raise ValueError("q, k, v must share shape, dtype and device")
+
+
+def num_blocks(heads, frames, tokens_per_frame, dtype=BF16) -> int:
+    p = problem(heads, frames, tokens_per_frame, dtype)
+    r = _lib().saf3r_num_blocks(ctypes.byref(p))
+    _check(min(r, 0), "saf3r_num_blocks")
+    return r
+
+
+def index_capacity(table, frames, tokens_per_frame, dtype=BF16) -> int:
+    p = problem(len(table), frames, tokens_per_frame, dtype)
+    r = _lib().saf3r_index_capacity(ctypes.byref(p), head_table(table))
+    _check(min(r, 0), "saf3r_index_capacity")
+    return r
+
+
+def estimate_blocks(q, k, table, frames, tokens_per_frame, q_pooled=None, k_pooled=None,
+                    stream=None):
+    """Pooled Q and K (float64 ``[heads, nb, 64]``; Top-K heads only)."""
+    import torch
+
+    _check_qkv(q, k)
+    H, N, _ = q.shape
+    if frames * tokens_per_frame != N or len(table) != H:
+        raise ValueError("frames * tokens_per_frame must equal N and len(table) the heads")
+    nb = -(-N // BLOCK)
+    if q_pooled is None:
+        q_pooled = torch.zeros((H, nb, HEAD_DIM), dtype=torch.float64, device=q.device)
+    if k_pooled is None:
+        k_pooled = torch.zeros((H, nb, HEAD_DIM), dtype=torch.float64, device=q.device)
+    p = problem(H, frames, tokens_per_frame, _torch_dtype_code(q))
+    _check(_lib().saf3r_estimate_blocks(ctypes.byref(p), head_table(table), _ptr(q), _ptr(k),
+                                        _ptr(q_pooled), _ptr(k_pooled), _stream(stream)),
+           "saf3r_estimate_blocks")
+    return q_pooled, k_pooled
+
+
+def select_blocks(q_pooled, k_pooled, table, frames, tokens_per_frame, cap=None,
+                  block_idx=None, block_cnt=None, want_scores=False, dtype=BF16, stream=None):
+    """Kept key-block lists: ``(block_idx [H, nb, cap], block_cnt [H, nb], scores or None)``."""
+    import torch
+
+    H, nb, _ = q_pooled.shape
+    for t in (q_pooled, k_pooled):
+        if not (t.is_cuda and t.is_contiguous() and t.dtype == torch.float64 and t.shape == (H, nb, HEAD_DIM)):
+            raise ValueError("pooled tensors must be contiguous float64 [heads, nb, 64] on the device")
+    if cap is None:
+        cap = index_capacity(table, frames, tokens_per_frame, dtype)
+    dev = q_pooled.device
+    if block_idx is None:
+        block_idx = torch.empty((H, nb, cap), dtype=torch.int32, device=dev)
+    if block_cnt is None:
+        block_cnt = torch.empty((H, nb), dtype=torch.int32, device=dev)
+    scores = torch.zeros((H, nb, nb), dtype=torch.float64, device=dev) if want_scores else None
+    p = problem(H, frames, tokens_per_frame, dtype)
+    _check(_lib().saf3r_select_blocks(ctypes.byref(p), head_table(table), _ptr(q_pooled),
+                                      _ptr(k_pooled), _ptr(block_idx), _ptr(block_cnt), int(cap),
+                                      _ptr(scores), _stream(stream)),
+           "saf3r_select_blocks")
+    return block_idx, block_cnt, scores
+
+
+def sparse_attention(q, k, v, table, frames, tokens_per_frame, block_idx=None, block_cnt=None,
+                     out=None, want_lse=False, stream=None):
+    """Attention over the kept blocks: ``(out [H, N, 64], lse [H, N] float32 or None)``."""
+    import torch
+
+    _check_qkv(q, k, v)
+    H, N, _ = q.shape
+    if frames * tokens_per_frame != N or len(table) != H:
+        raise ValueError("frames * tokens_per_frame must equal N and len(table) the heads")
+    cap = 0 if block_idx is None else int(block_idx.shape[2])
+    if out is None:
+        out = torch.empty_like(q)
+    lse = torch.empty((H, N), dtype=torch.float32, device=q.device) if want_lse else None
+    p = problem(H, frames, tokens_per_frame, _torch_dtype_code(q))
+    _check(_lib().saf3r_sparse_attention(ctypes.byref(p), head_table(table), _ptr(q), _ptr(k),
+                                         _ptr(v), _ptr(block_idx), _ptr(block_cnt), cap, _ptr(out),
+                                         _ptr(lse), _stream(stream)),
+           "saf3r_sparse_attention")
+    return out, lse
+
+
+def run_layer(q, k, v, table, frames, tokens_per_frame, stream=None):
+    """estimate -> select -> attend for one layer; returns (out, block_idx, block_cnt)."""
+    dtype = _torch_dtype_code(q)
+    qp, kp = estimate_blocks(q, k, table, frames, tokens_per_frame, stream=stream)
+    idx, cnt, _ = select_blocks(qp, kp, table, frames, tokens_per_frame, dtype=dtype, stream=stream)
+    out, _ = sparse_attention(q, k, v, table, frames, tokens_per_frame, idx, cnt, stream=stream)
+    return out, idx, cnt

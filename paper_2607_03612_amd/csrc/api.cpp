@@ -1,0 +1,231 @@
+// C ABI of the SAF3R hot path: host-side validation, launch geometry and
+// work ordering. Every check runs before any launch, so a call that returns
+// an error has enqueued nothing.
+#include <math.h>
+#include <stdint.h>
+
+#include <algorithm>
+#include <numeric>
+#include <vector>
+
+#include "../../include/saf3r.h"
+#include "saf3r_internal.h"
+
+namespace {
+
+using saf3r::kMaxBlocks;
+using saf3r::kMaxHeads;
+
+constexpr int64_t kMaxTokens = (int64_t)kMaxBlocks * saf3r::kBlock;  // 1,048,576
+
+// Problem sizes after validation.
+struct Shape {
+  int heads;
+  int64_t n;
+  int nb;
+  int tokens_per_frame;
+  int dtype;
+};
+
+saf3r_status check_problem(const saf3r_problem* p, Shape* out) {
+  if (!p) return SAF3R_ERR_INVALID_ARGUMENT;
+  if (p->heads <= 0 || p->frames <= 0 || p->tokens_per_frame <= 0) return SAF3R_ERR_INVALID_ARGUMENT;
+  if (p->dtype != SAF3R_F32 && p->dtype != SAF3R_BF16) return SAF3R_ERR_INVALID_ARGUMENT;
+  if (p->head_dim != saf3r::kHeadDim || p->block != saf3r::kBlock) return SAF3R_ERR_UNSUPPORTED;
+  if (p->heads > kMaxHeads) return SAF3R_ERR_UNSUPPORTED;
+  const int64_t n = (int64_t)p->frames * p->tokens_per_frame;
+  if (n > kMaxTokens) return SAF3R_ERR_UNSUPPORTED;
+  out->heads = p->heads;
+  out->n = n;
+  out->nb = (int)((n + saf3r::kBlock - 1) / saf3r::kBlock);
+  out->tokens_per_frame = p->tokens_per_frame;
+  out->dtype = p->dtype;
+  return SAF3R_OK;
+}
+
+saf3r_status check_table(const Shape& s, const saf3r_head_cfg* t) {
+  if (!t) return SAF3R_ERR_INVALID_ARGUMENT;
+  for (int h = 0; h < s.heads; ++h) {
+    switch (t[h].pattern) {
+      case SAF3R_DENSE:
+      case SAF3R_FRAME_LOCAL:
+        break;
+      case SAF3R_TOPK:
+        if (t[h].topk_blocks < 1 || t[h].topk_blocks > s.nb) return SAF3R_ERR_BAD_TABLE;
+        break;
+      default:
+        return SAF3R_ERR_BAD_TABLE;
+    }
+  }
+  return SAF3R_OK;
+}
+
+// Kept blocks of query block i of a frame-local head: the key blocks whose
+// tokens overlap the frames touched by block i (a contiguous range).
+int frame_local_len(const Shape& s, int i) {
+  const int64_t T = s.tokens_per_frame;
+  const int64_t first = (int64_t)i * saf3r::kBlock;
+  const int64_t last = std::min<int64_t>(first + saf3r::kBlock, s.n) - 1;
+  const int64_t tok_lo = (first / T) * T;
+  const int64_t tok_hi = std::min<int64_t>((last / T + 1) * T, s.n) - 1;
+  return (int)(tok_hi / saf3r::kBlock - tok_lo / saf3r::kBlock + 1);
+}
+
+int max_frame_local_len(const Shape& s) {
+  int best = 0;
+  for (int i = 0; i < s.nb; ++i) best = std::max(best, frame_local_len(s, i));
+  return best;
+}
+
+int capacity(const Shape& s, const saf3r_head_cfg* t) {
+  int cap = 1;
+  bool any_fl = false;
+  for (int h = 0; h < s.heads; ++h) {
+    if (t[h].pattern == SAF3R_TOPK) cap = std::max(cap, t[h].topk_blocks);
+    if (t[h].pattern == SAF3R_FRAME_LOCAL) any_fl = true;
+  }
+  if (any_fl) cap = std::max(cap, max_frame_local_len(s));
+  return cap;
+}
+
+saf3r_status hip_status(hipError_t e) { return e == hipSuccess ? SAF3R_OK : SAF3R_ERR_HIP; }
+
+}  // namespace
+
+extern "C" {
+
+int32_t saf3r_num_blocks(const saf3r_problem* problem) {
+  Shape s;
+  const saf3r_status st = check_problem(problem, &s);
+  return st == SAF3R_OK ? s.nb : (int32_t)st;
+}
+
+int32_t saf3r_index_capacity(const saf3r_problem* problem, const saf3r_head_cfg* table) {
+  Shape s;
+  saf3r_status st = check_problem(problem, &s);
+  if (st != SAF3R_OK) return st;
+  st = check_table(s, table);
+  if (st != SAF3R_OK) return st;
+  return capacity(s, table);
+}
+
+saf3r_status saf3r_estimate_blocks(const saf3r_problem* problem, const saf3r_head_cfg* table,
+                                   const void* q, const void* k, double* q_pooled,
+                                   double* k_pooled, void* stream) {
+  Shape s;
+  saf3r_status st = check_problem(problem, &s);
+  if (st != SAF3R_OK) return st;
+  st = check_table(s, table);
+  if (st != SAF3R_OK) return st;
+  if (!q || !k || !q_pooled || !k_pooled) return SAF3R_ERR_INVALID_ARGUMENT;
+  saf3r::PoolArgs a{};
+  a.n = s.n;
+  a.nb = s.nb;
+  for (int h = 0; h < s.heads; ++h)
+    if (table[h].pattern == SAF3R_TOPK) a.head[a.n_heads++] = (int16_t)h;
+  return hip_status(saf3r::launch_pool(s.dtype, q, k, q_pooled, k_pooled, a,
+                                       static_cast<hipStream_t>(stream)));
+}
+
+saf3r_status saf3r_select_blocks(const saf3r_problem* problem, const saf3r_head_cfg* table,
+                                 const double* q_pooled, const double* k_pooled,
+                                 int32_t* block_idx, int32_t* block_cnt, int32_t cap,
+                                 double* scores_or_null, void* stream) {
+  Shape s;
+  saf3r_status st = check_problem(problem, &s);
+  if (st != SAF3R_OK) return st;
+  st = check_table(s, table);
+  if (st != SAF3R_OK) return st;
+  if (!q_pooled || !k_pooled || !block_idx || !block_cnt) return SAF3R_ERR_INVALID_ARGUMENT;
+  if (cap < capacity(s, table)) return SAF3R_ERR_CAPACITY;
+
+  saf3r::TopKArgs ta{};
+  ta.n = s.n;
+  ta.nb = s.nb;
+  ta.cap = cap;
+  saf3r::StaticArgs sa{};
+  sa.n = s.n;
+  sa.nb = s.nb;
+  sa.cap = cap;
+  sa.tokens_per_frame = s.tokens_per_frame;
+  for (int h = 0; h < s.heads; ++h) {
+    if (table[h].pattern == SAF3R_TOPK) {
+      ta.head[ta.n_heads] = (int16_t)h;
+      ta.topk[ta.n_heads++] = table[h].topk_blocks;
+    } else {
+      sa.head[sa.n_heads] = (int16_t)h;
+      sa.pattern[sa.n_heads++] = (int8_t)table[h].pattern;
+    }
+  }
+  // Rows scored per workgroup: as many as fit while two workgroups share a
+  // CU's 160 KB of LDS, else as many as fit at all.
+  constexpr size_t kLdsPerCu = 160 * 1024;
+  int rows = 8;
+  while (rows > 1 && saf3r::topk_lds_bytes(rows, s.nb) > kLdsPerCu / 2) rows /= 2;
+  ta.rows_per_group = rows;
+  const size_t lds = saf3r::topk_lds_bytes(rows, s.nb);
+  if (lds > kLdsPerCu) return SAF3R_ERR_UNSUPPORTED;
+
+  hipStream_t hs = static_cast<hipStream_t>(stream);
+  hipError_t e = saf3r::launch_select_static(block_idx, block_cnt, sa, hs);
+  if (e != hipSuccess) return SAF3R_ERR_HIP;
+  e = saf3r::launch_select_topk(q_pooled, k_pooled, block_idx, block_cnt, scores_or_null, ta,
+                                lds, hs);
+  return hip_status(e);
+}
+
+saf3r_status saf3r_sparse_attention(const saf3r_problem* problem, const saf3r_head_cfg* table,
+                                    const void* q, const void* k, const void* v,
+                                    const int32_t* block_idx, const int32_t* block_cnt,
+                                    int32_t cap, void* out, float* lse_or_null, void* stream) {
+  Shape s;
+  saf3r_status st = check_problem(problem, &s);
+  if (st != SAF3R_OK) return st;
+  st = check_table(s, table);
+  if (st != SAF3R_OK) return st;
+  if (!q || !k || !v || !out) return SAF3R_ERR_INVALID_ARGUMENT;
+  bool all_dense = true;
+  for (int h = 0; h < s.heads; ++h) all_dense = all_dense && table[h].pattern == SAF3R_DENSE;
+  if (!all_dense) {
+    if (!block_idx || !block_cnt) return SAF3R_ERR_INVALID_ARGUMENT;
+    if (cap < capacity(s, table)) return SAF3R_ERR_CAPACITY;
+  }
+
+  saf3r::AttnArgs a{};
+  a.n = s.n;
+  a.nb = s.nb;
+  a.cap = cap;
+  a.heads = s.heads;
+  a.slab = (s.nb + 7) / 8;
+  a.scale_log2 = (float)(1.4426950408889634 / sqrt((double)saf3r::kHeadDim));
+  // heads in decreasing per-row cost (kept blocks per query block), so the
+  // longest rows start first
+  std::vector<int> cost(s.heads);
+  const int fl_len = max_frame_local_len(s);
+  for (int h = 0; h < s.heads; ++h) {
+    const int p = table[h].pattern;
+    a.dense[h] = p == SAF3R_DENSE ? 1 : 0;
+    cost[h] = p == SAF3R_DENSE ? s.nb : (p == SAF3R_TOPK ? table[h].topk_blocks : fl_len);
+  }
+  std::vector<int> order(s.heads);
+  std::iota(order.begin(), order.end(), 0);
+  std::stable_sort(order.begin(), order.end(), [&](int x, int y) { return cost[x] > cost[y]; });
+  for (int hh = 0; hh < s.heads; ++hh) a.order[hh] = (int16_t)order[hh];
+
+  return hip_status(saf3r::launch_attention(s.dtype, q, k, v, block_idx, block_cnt, out,
+                                            lse_or_null, a, static_cast<hipStream_t>(stream)));
+}
+
+const char* saf3r_status_string(int32_t status) {
+  switch (status) {
+    case SAF3R_OK: return "ok";
+    case SAF3R_ERR_INVALID_ARGUMENT: return "invalid argument (null pointer, size or dtype)";
+    case SAF3R_ERR_UNSUPPORTED: return "unsupported (head_dim/block must be 64; size limits)";
+    case SAF3R_ERR_CAPACITY: return "index capacity smaller than saf3r_index_capacity()";
+    case SAF3R_ERR_HIP: return "HIP runtime error on launch";
+    case SAF3R_ERR_BAD_TABLE: return "bad pattern table (class or Top-K budget)";
+    default: return "unknown status";
+  }
+}
+
+}  // extern "C"

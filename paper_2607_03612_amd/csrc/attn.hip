@@ -1,0 +1,446 @@
+// Block-sparse attention over the kept key blocks (Sec. 4.1: the Top-K and
+// static kernels compute only the scores between the queries and the
+// selected keys, and the softmax is renormalised over that set), with the
+// dense ("Full") case as the same loop over every key block.
+//
+// One wave owns one (head, 64-query block) and walks its kept-block list with
+// an online softmax:
+//   S^T = K Q^T      (keys x queries) on MFMA, so a lane owns one query
+//                    column and the row max / row sum stay inside the lane
+//                    pair (lane, lane ^ 32);
+//   O^T += V^T P^T   (head dim x queries) on MFMA, P^T taken straight from
+//                    the S^T accumulators, V^T read from LDS with the gfx950
+//                    transposing LDS read so V is never transposed in memory.
+// Q sits in registers for the whole loop, K tiles are loaded straight into
+// the MFMA operand layout (prefetched one tile ahead), V goes through a
+// per-wave LDS tile. All global accesses use buffer instructions bounded by
+// the head's extent, so a partial last block reads zeros and a corrupt index
+// list cannot touch memory outside the head.
+//
+// Launch order: workgroup b runs on XCD b % 8; each XCD takes a contiguous
+// slab of query blocks of every head (neighbouring query blocks share kept
+// key blocks, which then hit in that XCD's L2), heads in decreasing cost.
+#include "saf3r_internal.h"
+
+namespace saf3r {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+typedef int i32x2 __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+
+constexpr uint32_t kRsrcWord3 = 0x00020000u;  // gfx9 buffer descriptor: 32-bit raw data
+constexpr int kVStride = 72;                   // bf16 per LDS row of V: 64 + 8 pad
+constexpr int kFStride = 65;                   // fp32 per LDS row (fp32 path)
+constexpr float kNegInf = -__builtin_inff();
+constexpr float kLn2 = 0.6931471805599453f;
+
+__device__ inline __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes,
+                                           (int)kRsrcWord3);
+}
+
+__device__ inline bf16x8 load_b128(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
+  return __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(r, (int)byte_off, 0, 0));
+}
+
+__device__ inline float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+struct Work {
+  int h, i;
+  bool valid;
+};
+
+__device__ inline Work work_item(const AttnArgs& a) {
+  const int xcd = blockIdx.x & 7;
+  const int u = blockIdx.x >> 3;
+  const int hh = u / a.slab;
+  const int i = xcd * a.slab + (u - hh * a.slab);
+  Work w;
+  w.valid = hh < a.heads && i < a.nb;
+  w.h = w.valid ? a.order[hh] : 0;
+  w.i = i;
+  return w;
+}
+
+// ------------------------------------------------------------------ bf16
+
+// K tile j as the A operand of v_mfma_f32_32x32x16_bf16: rows = keys.
+// kA[tk][s]: key 64j + 32tk + (lane % 32), head dims 16s + 8(lane / 32) + [0, 8).
+__device__ inline void load_k_tile(bf16x8 (&kA)[2][4], __amdgpu_buffer_rsrc_t rk, int j,
+                                   int l32, int hf) {
+#pragma unroll
+  for (int tk = 0; tk < 2; ++tk)
+#pragma unroll
+    for (int s = 0; s < 4; ++s)
+      kA[tk][s] = load_b128(
+          rk, (uint32_t)(((j * kBlock + 32 * tk + l32) * kHeadDim + 16 * s + 8 * hf) * 2));
+}
+
+__global__ __launch_bounds__(64) void attn_bf16_kernel(const uint16_t* __restrict__ q,
+                                                      const uint16_t* __restrict__ k,
+                                                      const uint16_t* __restrict__ v,
+                                                      const int32_t* __restrict__ idx,
+                                                      const int32_t* __restrict__ cnt,
+                                                      uint16_t* __restrict__ out,
+                                                      float* __restrict__ lse, AttnArgs a) {
+  __shared__ __attribute__((aligned(16))) __bf16 vs[kBlock * kVStride];
+
+  const Work w = work_item(a);
+  if (!w.valid) return;
+  const int lane = threadIdx.x;
+  const int l32 = lane & 31;
+  const int hf = lane >> 5;
+  const int nb = a.nb;
+  const bool dense = a.dense[w.h] != 0;
+  const int32_t* list = idx + ((int64_t)w.h * nb + w.i) * a.cap;
+  int count = nb;
+  if (!dense) count = min(max(cnt[(int64_t)w.h * nb + w.i], 0), a.cap);
+
+  const int64_t head_off = (int64_t)w.h * a.n * kHeadDim;
+  const uint32_t head_bytes = (uint32_t)(a.n * kHeadDim * 2);
+  const __amdgpu_buffer_rsrc_t rq = make_rsrc(q + head_off, head_bytes);
+  const __amdgpu_buffer_rsrc_t rk = make_rsrc(k + head_off, head_bytes);
+  const __amdgpu_buffer_rsrc_t rv = make_rsrc(v + head_off, head_bytes);
+  const __amdgpu_buffer_rsrc_t ro = make_rsrc(out + head_off, head_bytes);
+
+  // Q^T as the B operand: qB[tq][s] = Q[64i + 32tq + l32][16s + 8hf + (0..7)]
+  bf16x8 qB[2][4];
+#pragma unroll
+  for (int tq = 0; tq < 2; ++tq)
+#pragma unroll
+    for (int s = 0; s < 4; ++s)
+      qB[tq][s] = load_b128(
+          rq, (uint32_t)(((w.i * kBlock + 32 * tq + l32) * kHeadDim + 16 * s + 8 * hf) * 2));
+
+  f32x16 o[2][2];  // O^T tiles [head-dim half c][query half tq]
+#pragma unroll
+  for (int c = 0; c < 2; ++c)
+#pragma unroll
+    for (int tq = 0; tq < 2; ++tq)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) o[c][tq][e] = 0.f;
+  float m[2] = {kNegInf, kNegInf};  // running max of the log2-scaled scores
+  float l[2] = {0.f, 0.f};          // this lane's share of the running row sum
+
+  const bool tail = (a.n % kBlock) != 0;
+  const float sc = a.scale_log2;
+
+  // transposing-read addresses (element offsets in vs) for V^T operands
+  const int tr_row = 4 * hf + ((lane & 15) >> 2);
+  const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+
+  bf16x8 kA[2][4];
+  int j = count > 0 ? (dense ? 0 : list[0]) : 0;
+  load_k_tile(kA, rk, j, l32, hf);
+
+  for (int it = 0; it < count; ++it) {
+    // V tile j: rows 8n + lane/8, 16-byte chunk lane%8 (coalesced 1 KB per load)
+    i32x4 vreg[8];
+#pragma unroll
+    for (int n8 = 0; n8 < 8; ++n8)
+      vreg[n8] = __builtin_amdgcn_raw_buffer_load_b128(
+          rv, (int)(((j * kBlock + 8 * n8 + (lane >> 3)) * kHeadDim + (lane & 7) * 8) * 2), 0, 0);
+
+    // S^T[tk][tq] (keys 32tk.., queries 32tq..)
+    f32x16 s[2][2];
+#pragma unroll
+    for (int tk = 0; tk < 2; ++tk)
+#pragma unroll
+      for (int tq = 0; tq < 2; ++tq) {
+        f32x16 acc = {};
+#pragma unroll
+        for (int st = 0; st < 4; ++st)
+          acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kA[tk][st], qB[tq][st], acc, 0, 0, 0);
+        s[tk][tq] = acc;
+      }
+
+    const int jcur = j;
+    if (it + 1 < count) {
+      j = dense ? it + 1 : list[it + 1];
+      load_k_tile(kA, rk, j, l32, hf);
+    }
+
+    if (tail && jcur == nb - 1) {
+      const int valid_keys = (int)(a.n - (int64_t)jcur * kBlock);
+#pragma unroll
+      for (int tk = 0; tk < 2; ++tk)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int key = 32 * tk + 8 * (e >> 2) + 4 * hf + (e & 3);
+          if (key >= valid_keys) {
+            s[tk][0][e] = kNegInf;
+            s[tk][1][e] = kNegInf;
+          }
+        }
+    }
+
+    // online softmax per query column (this lane and lane ^ 32 share it)
+#pragma unroll
+    for (int tq = 0; tq < 2; ++tq) {
+      float mx = s[0][tq][0];
+#pragma unroll
+      for (int e = 1; e < 16; ++e) mx = fmaxf(mx, s[0][tq][e]);
+#pragma unroll
+      for (int e = 0; e < 16; ++e) mx = fmaxf(mx, s[1][tq][e]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      const float mnew = fmaxf(m[tq], mx * sc);
+      const float alpha = fast_exp2(m[tq] - mnew);
+      m[tq] = mnew;
+      float rs = 0.f;
+#pragma unroll
+      for (int tk = 0; tk < 2; ++tk)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const float p = fast_exp2(fmaf(s[tk][tq][e], sc, -mnew));
+          s[tk][tq][e] = p;
+          rs += p;
+        }
+      l[tq] = fmaf(l[tq], alpha, rs);
+#pragma unroll
+      for (int c = 0; c < 2; ++c) o[c][tq] *= alpha;
+    }
+
+    // stage V in LDS (same wave wrote and reads it: no barrier needed)
+#pragma unroll
+    for (int n8 = 0; n8 < 8; ++n8)
+      *reinterpret_cast<i32x4*>(&vs[(8 * n8 + (lane >> 3)) * kVStride + (lane & 7) * 8]) = vreg[n8];
+
+    // O^T[c][tq] += V^T[c][keys] P^T[keys][tq]
+#pragma unroll
+    for (int tk = 0; tk < 2; ++tk)
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        bf16x8 pB[2];
+#pragma unroll
+        for (int tq = 0; tq < 2; ++tq)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) pB[tq][e] = (__bf16)s[tk][tq][8 * u + e];
+        const int krow = 32 * tk + 16 * u + tr_row;
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+          const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+              (lds_bf16x4*)(&vs[krow * kVStride + 32 * c + tr_col]));
+          const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+              (lds_bf16x4*)(&vs[(krow + 8) * kVStride + 32 * c + tr_col]));
+          const bf16x8 vA = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+#pragma unroll
+          for (int tq = 0; tq < 2; ++tq)
+            o[c][tq] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vA, pB[tq], o[c][tq], 0, 0, 0);
+        }
+      }
+  }
+
+  // epilogue: normalise, round to bf16, store; log-sum-exp in natural log
+#pragma unroll
+  for (int tq = 0; tq < 2; ++tq) {
+    const float lt = l[tq] + __shfl_xor(l[tq], 32);
+    const float inv = 1.0f / lt;
+    const int query = w.i * kBlock + 32 * tq + l32;
+#pragma unroll
+    for (int c = 0; c < 2; ++c)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        bf16x4 ov;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) ov[r] = (__bf16)(o[c][tq][4 * g + r] * inv);
+        __builtin_amdgcn_raw_buffer_store_b64(
+            __builtin_bit_cast(i32x2, ov), ro,
+            (int)((query * kHeadDim + 32 * c + 8 * g + 4 * hf) * 2), 0, 0);
+      }
+    if (lse && hf == 0 && query < a.n)
+      lse[(int64_t)w.h * a.n + query] = (m[tq] + __log2f(lt)) * kLn2;
+  }
+}
+
+// ------------------------------------------------------------------ fp32
+
+// Same structure with v_mfma_f32_32x32x2_f32 and fp32 softmax operands; K and
+// V tiles both go through LDS (one wave, no barrier).
+__global__ __launch_bounds__(64) void attn_f32_kernel(const float* __restrict__ q,
+                                                     const float* __restrict__ k,
+                                                     const float* __restrict__ v,
+                                                     const int32_t* __restrict__ idx,
+                                                     const int32_t* __restrict__ cnt,
+                                                     float* __restrict__ out,
+                                                     float* __restrict__ lse, AttnArgs a) {
+  __shared__ float ks[kBlock * kFStride];
+  __shared__ float vsf[kBlock * kFStride];
+
+  const Work w = work_item(a);
+  if (!w.valid) return;
+  const int lane = threadIdx.x;
+  const int l32 = lane & 31;
+  const int hf = lane >> 5;
+  const int nb = a.nb;
+  const bool dense = a.dense[w.h] != 0;
+  const int32_t* list = idx + ((int64_t)w.h * nb + w.i) * a.cap;
+  int count = nb;
+  if (!dense) count = min(max(cnt[(int64_t)w.h * nb + w.i], 0), a.cap);
+
+  const int64_t head_off = (int64_t)w.h * a.n * kHeadDim;
+  const uint32_t head_bytes = (uint32_t)(a.n * kHeadDim * 4);
+  const __amdgpu_buffer_rsrc_t rq = make_rsrc(q + head_off, head_bytes);
+  const __amdgpu_buffer_rsrc_t rk = make_rsrc(k + head_off, head_bytes);
+  const __amdgpu_buffer_rsrc_t rv = make_rsrc(v + head_off, head_bytes);
+  const __amdgpu_buffer_rsrc_t ro = make_rsrc(out + head_off, head_bytes);
+
+  // Q^T B operand: qB[tq][s] = Q[64i + 32tq + l32][2s + hf]
+  float qB[2][32];
+#pragma unroll
+  for (int tq = 0; tq < 2; ++tq)
+#pragma unroll
+    for (int s4 = 0; s4 < 8; ++s4) {
+      // dims 8*s4 .. 8*s4+7 of this query: the lane half picks odd or even
+      const int row = w.i * kBlock + 32 * tq + l32;
+      const f32x4 x0 = __builtin_bit_cast(
+          f32x4, __builtin_amdgcn_raw_buffer_load_b128(rq, (row * kHeadDim + 8 * s4) * 4, 0, 0));
+      const f32x4 x1 = __builtin_bit_cast(
+          f32x4, __builtin_amdgcn_raw_buffer_load_b128(rq, (row * kHeadDim + 8 * s4 + 4) * 4, 0, 0));
+      qB[tq][4 * s4 + 0] = hf ? x0[1] : x0[0];
+      qB[tq][4 * s4 + 1] = hf ? x0[3] : x0[2];
+      qB[tq][4 * s4 + 2] = hf ? x1[1] : x1[0];
+      qB[tq][4 * s4 + 3] = hf ? x1[3] : x1[2];
+    }
+
+  f32x16 o[2][2];
+#pragma unroll
+  for (int c = 0; c < 2; ++c)
+#pragma unroll
+    for (int tq = 0; tq < 2; ++tq)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) o[c][tq][e] = 0.f;
+  float m[2] = {kNegInf, kNegInf};
+  float l[2] = {0.f, 0.f};
+  const bool tail = (a.n % kBlock) != 0;
+  const float sc = a.scale_log2;
+
+  for (int it = 0; it < count; ++it) {
+    const int j = dense ? it : list[it];
+    // stage K and V tiles: rows 4n + lane/16, float4 chunk lane%16
+#pragma unroll
+    for (int n4 = 0; n4 < 16; ++n4) {
+      const int row = 4 * n4 + (lane >> 4);
+      const int off = ((j * kBlock + row) * kHeadDim + (lane & 15) * 4) * 4;
+      const f32x4 kx = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rk, off, 0, 0));
+      const f32x4 vx = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rv, off, 0, 0));
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        ks[row * kFStride + (lane & 15) * 4 + e] = kx[e];
+        vsf[row * kFStride + (lane & 15) * 4 + e] = vx[e];
+      }
+    }
+
+    f32x16 s[2][2];
+#pragma unroll
+    for (int tk = 0; tk < 2; ++tk)
+#pragma unroll
+      for (int tq = 0; tq < 2; ++tq) {
+        f32x16 acc = {};
+#pragma unroll
+        for (int st = 0; st < 32; ++st)
+          acc = __builtin_amdgcn_mfma_f32_32x32x2f32(ks[(32 * tk + l32) * kFStride + 2 * st + hf],
+                                                     qB[tq][st], acc, 0, 0, 0);
+        s[tk][tq] = acc;
+      }
+
+    if (tail && j == nb - 1) {
+      const int valid_keys = (int)(a.n - (int64_t)j * kBlock);
+#pragma unroll
+      for (int tk = 0; tk < 2; ++tk)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int key = 32 * tk + 8 * (e >> 2) + 4 * hf + (e & 3);
+          if (key >= valid_keys) {
+            s[tk][0][e] = kNegInf;
+            s[tk][1][e] = kNegInf;
+          }
+        }
+    }
+
+#pragma unroll
+    for (int tq = 0; tq < 2; ++tq) {
+      float mx = s[0][tq][0];
+#pragma unroll
+      for (int e = 1; e < 16; ++e) mx = fmaxf(mx, s[0][tq][e]);
+#pragma unroll
+      for (int e = 0; e < 16; ++e) mx = fmaxf(mx, s[1][tq][e]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      const float mnew = fmaxf(m[tq], mx * sc);
+      const float alpha = exp2f(m[tq] - mnew);
+      m[tq] = mnew;
+      float rs = 0.f;
+#pragma unroll
+      for (int tk = 0; tk < 2; ++tk)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const float p = exp2f(fmaf(s[tk][tq][e], sc, -mnew));
+          s[tk][tq][e] = p;
+          rs += p;
+        }
+      l[tq] = fmaf(l[tq], alpha, rs);
+#pragma unroll
+      for (int c = 0; c < 2; ++c) o[c][tq] *= alpha;
+    }
+
+    // O^T[c][tq] += V^T P^T; k-step (tk, g, r) pairs key 32tk+8g+r (lane half
+    // 0) with key 32tk+8g+4+r (lane half 1), i.e. S^T register 4g+r.
+#pragma unroll
+    for (int c = 0; c < 2; ++c)
+#pragma unroll
+      for (int tk = 0; tk < 2; ++tk)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int key = 32 * tk + 8 * (e >> 2) + 4 * hf + (e & 3);
+          const float va = vsf[key * kFStride + 32 * c + l32];
+#pragma unroll
+          for (int tq = 0; tq < 2; ++tq)
+            o[c][tq] = __builtin_amdgcn_mfma_f32_32x32x2f32(va, s[tk][tq][e], o[c][tq], 0, 0, 0);
+        }
+  }
+
+#pragma unroll
+  for (int tq = 0; tq < 2; ++tq) {
+    const float lt = l[tq] + __shfl_xor(l[tq], 32);
+    const float inv = 1.0f / lt;
+    const int query = w.i * kBlock + 32 * tq + l32;
+#pragma unroll
+    for (int c = 0; c < 2; ++c)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        f32x4 ov;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) ov[r] = o[c][tq][4 * g + r] * inv;
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(i32x4, ov), ro,
+                                               (query * kHeadDim + 32 * c + 8 * g + 4 * hf) * 4, 0, 0);
+      }
+    if (lse && hf == 0 && query < a.n)
+      lse[(int64_t)w.h * a.n + query] = (m[tq] + log2f(lt)) * kLn2;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_attention(int dtype, const void* q, const void* k, const void* v,
+                            const int32_t* idx, const int32_t* cnt, void* out, float* lse,
+                            const AttnArgs& a, hipStream_t s) {
+  const int64_t groups = 8LL * a.heads * a.slab;
+  if (groups == 0) return hipSuccess;
+  if (dtype == 1) {
+    hipLaunchKernelGGL(attn_bf16_kernel, dim3((unsigned)groups), dim3(64), 0, s,
+                       static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
+                       static_cast<const uint16_t*>(v), idx, cnt, static_cast<uint16_t*>(out),
+                       lse, a);
+  } else {
+    hipLaunchKernelGGL(attn_f32_kernel, dim3((unsigned)groups), dim3(64), 0, s,
+                       static_cast<const float*>(q), static_cast<const float*>(k),
+                       static_cast<const float*>(v), idx, cnt, static_cast<float*>(out), lse, a);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace saf3r

@@ -1,0 +1,68 @@
+// Internal declarations shared by the gfx950 kernels and the C ABI layer.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace saf3r {
+
+constexpr int kHeadDim = 64;
+constexpr int kBlock = 64;
+constexpr int kMaxHeads = 256;
+constexpr int kMaxBlocks = 16384;  // select keeps one score row per query block in LDS
+
+enum Pattern : int32_t { kDense = 0, kFrameLocal = 1, kTopK = 2 };
+
+// ---------------------------------------------------------------- launches
+
+struct PoolArgs {
+  int64_t n;            // tokens per head
+  int32_t nb;           // blocks per head
+  int32_t n_heads;      // heads to pool (the Top-K heads)
+  int16_t head[kMaxHeads];
+};
+
+struct TopKArgs {
+  int64_t n;
+  int32_t nb;
+  int32_t cap;
+  int32_t rows_per_group;  // query blocks scored together by one workgroup
+  int32_t n_heads;
+  int16_t head[kMaxHeads];
+  int32_t topk[kMaxHeads];
+};
+
+struct StaticArgs {
+  int64_t n;
+  int32_t nb;
+  int32_t cap;
+  int32_t tokens_per_frame;
+  int32_t n_heads;
+  int16_t head[kMaxHeads];
+  int8_t pattern[kMaxHeads];
+};
+
+struct AttnArgs {
+  int64_t n;
+  int32_t nb;
+  int32_t cap;
+  int32_t heads;
+  int32_t slab;           // query blocks of one head handled by one XCD: ceil(nb / 8)
+  float scale_log2;       // log2(e) / sqrt(64)
+  int16_t order[kMaxHeads];   // heads, most expensive first
+  int8_t dense[kMaxHeads];    // per head: 1 = iterate all key blocks
+};
+
+hipError_t launch_pool(int dtype, const void* q, const void* k, double* qp, double* kp,
+                       const PoolArgs& a, hipStream_t s);
+hipError_t launch_select_topk(const double* qp, const double* kp, int32_t* idx, int32_t* cnt,
+                              double* scores, const TopKArgs& a, size_t lds_bytes, hipStream_t s);
+hipError_t launch_select_static(int32_t* idx, int32_t* cnt, const StaticArgs& a, hipStream_t s);
+hipError_t launch_attention(int dtype, const void* q, const void* k, const void* v,
+                            const int32_t* idx, const int32_t* cnt, void* out, float* lse,
+                            const AttnArgs& a, hipStream_t s);
+
+// Bytes of LDS the Top-K selection kernel needs for `rows` query blocks.
+size_t topk_lds_bytes(int rows, int nb);
+
+}  // namespace saf3r

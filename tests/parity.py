@@ -1,0 +1,94 @@
+"""Helpers shared by the GPU parity tests: upload, run through the C ABI,
+compare against the oracle. Holds none of the method's arithmetic."""
+import math
+
+import numpy as np
+
+NEAR_TIE = 1e-6          # selection must be exact where the oracle margin exceeds this
+TOL_BF16 = 2e-2          # max-abs error of bf16 outputs against the fp64 oracle
+TOL_F32 = 1e-4           # max-abs error of fp32 outputs against the fp64 oracle
+# Log-sum-exp: both dtypes accumulate the 64 products of q.k in fp32 (unit
+# roundoff 6e-8); with |q||k| up to ~200 on these inputs the score error is
+# ~1e-5 typical and bounded by ~1e-4, which the log-sum-exp inherits.
+LSE_TOL_BF16 = 2e-3
+LSE_TOL_F32 = 1e-4
+
+
+def to_device(x, dtype):
+    import torch
+
+    if dtype == "bf16":
+        return torch.from_numpy(x.view(np.int16)).cuda().view(torch.bfloat16)
+    return torch.from_numpy(x).cuda()
+
+
+def out_to_numpy(t):
+    import torch
+
+    return t.float().cpu().numpy().astype(np.float64) if t.dtype == torch.bfloat16 else \
+        t.cpu().numpy().astype(np.float64)
+
+
+def gpu_layer(P, w, q, k, v, table, want_scores=False, want_lse=True):
+    """Runs estimate -> select -> attend through the binding; returns numpy results."""
+    import torch
+
+    tq, tk, tv = (to_device(x, w.dtype) for x in (q, k, v))
+    qp, kp = P.estimate_blocks(tq, tk, table, w.frames, w.tokens_per_frame)
+    code = P.BF16 if w.dtype == "bf16" else P.F32
+    idx, cnt, scores = P.select_blocks(qp, kp, table, w.frames, w.tokens_per_frame,
+                                       want_scores=want_scores, dtype=code)
+    out, lse = P.sparse_attention(tq, tk, tv, table, w.frames, w.tokens_per_frame, idx, cnt,
+                                  want_lse=want_lse)
+    torch.cuda.synchronize()
+    res = {
+        "q_pooled": qp.cpu().numpy(), "k_pooled": kp.cpu().numpy(),
+        "idx": idx.cpu().numpy(), "cnt": cnt.cpu().numpy(),
+        "out": out_to_numpy(out), "lse": None if lse is None else lse.cpu().numpy().astype(np.float64),
+        "scores": None if scores is None else scores.cpu().numpy(),
+    }
+    return res
+
+
+def gpu_list(res, h, i):
+    c = int(res["cnt"][h, i])
+    return res["idx"][h, i, :c]
+
+
+def check_lists(res, h, i, pattern, oracle_list, margin, nb, cap):
+    """Returns 'ok', 'near_tie' or raises AssertionError with the row named."""
+    c = int(res["cnt"][h, i])
+    if pattern == 0:  # DENSE: count only, list not materialised
+        assert c == nb, f"head {h} block {i}: dense count {c} != {nb}"
+        return "ok"
+    row = res["idx"][h, i]
+    assert np.all(row[c:] == -1), f"head {h} block {i}: padding not -1"
+    got = row[:c]
+    assert np.all(np.diff(got) > 0), f"head {h} block {i}: list not strictly ascending"
+    assert got.min() >= 0 and got.max() < nb
+    if margin <= NEAR_TIE:
+        assert c == len(oracle_list)
+        return "near_tie"
+    assert c == len(oracle_list) and np.array_equal(got, oracle_list), \
+        f"head {h} block {i}: gpu {list(got)} != oracle {list(oracle_list)} (margin {margin})"
+    return "ok"
+
+
+def max_abs(a, b):
+    return float(np.max(np.abs(a - b))) if a.size else 0.0
+
+
+def sample_blocks(nb, count, seed):
+    """Seeded sample of query blocks that always includes the first and last."""
+    g = np.random.default_rng(seed)
+    pick = set(g.choice(nb, size=min(count, nb), replace=False).tolist())
+    pick |= {0, nb - 1}
+    return sorted(pick)
+
+
+def finite(x):
+    return bool(np.all(np.isfinite(x)))
+
+
+__all__ = ["NEAR_TIE", "TOL_BF16", "TOL_F32", "gpu_layer", "check_lists", "max_abs",
+           "sample_blocks", "to_device", "out_to_numpy", "gpu_list", "math"]

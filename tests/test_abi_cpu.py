@@ -1,0 +1,104 @@
+"""The C ABI on the host: the library loads, exports every declared symbol,
+and rejects bad arguments with a status code before anything is launched
+(none of these calls reaches the GPU)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "saf3r.h")
+
+
+@pytest.fixture(scope="module")
+def B():
+    from paper_2607_03612_amd import binding
+
+    if not os.path.exists(binding.LIB_PATH):
+        from paper_2607_03612_amd import build
+
+        build.build()
+    binding.load()
+    return binding
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[\w\s\*]*?\b(saf3r_\w+)\s*\(", text, re.M)))
+
+
+def test_header_declares_the_three_hot_path_calls():
+    names = declared_functions()
+    for n in ("saf3r_estimate_blocks", "saf3r_select_blocks", "saf3r_sparse_attention"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol(B):
+    lib = ctypes.CDLL(B.LIB_PATH)
+    names = declared_functions()
+    assert set(names) == set(B.EXPORTS)
+    for n in names:
+        assert hasattr(lib, n), f"{n} is declared but not exported"
+
+
+def _p(B, heads=16, frames=8, T=1374, head_dim=64, block=64, dtype=1):
+    return B.Problem(heads, frames, T, head_dim, block, dtype)
+
+
+def test_problem_validation(B):
+    lib = B.load()
+    nb = lib.saf3r_num_blocks
+    assert nb(ctypes.byref(_p(B))) == 172
+    assert nb(None) == -1
+    assert nb(ctypes.byref(_p(B, heads=0))) == -1
+    assert nb(ctypes.byref(_p(B, frames=-1))) == -1
+    assert nb(ctypes.byref(_p(B, dtype=7))) == -1
+    assert nb(ctypes.byref(_p(B, head_dim=128))) == -2
+    assert nb(ctypes.byref(_p(B, block=128))) == -2
+    assert nb(ctypes.byref(_p(B, heads=257))) == -2
+    assert nb(ctypes.byref(_p(B, frames=1024, T=1025))) == -2  # > 2^20 tokens
+    assert nb(ctypes.byref(_p(B, frames=1024, T=1024))) == 16384
+
+
+def test_table_validation_and_capacity(B):
+    lib = B.load()
+    cap = lib.saf3r_index_capacity
+    p = _p(B, heads=3, frames=8, T=1374)
+    assert cap(ctypes.byref(p), B.head_table([(0, 0), (1, 0), (2, 13)])) == 44
+    assert cap(ctypes.byref(p), B.head_table([(0, 0), (0, 0), (2, 100)])) == 100
+    assert cap(ctypes.byref(p), B.head_table([(0, 0)] * 3)) == 1
+    assert cap(ctypes.byref(p), B.head_table([(0, 0), (2, 0), (2, 1)])) == -5
+    assert cap(ctypes.byref(p), B.head_table([(0, 0), (2, 173), (2, 1)])) == -5
+    assert cap(ctypes.byref(p), B.head_table([(0, 0), (3, 1), (2, 1)])) == -5
+    assert cap(ctypes.byref(p), None) == -1
+    # frames of 128 tokens align with blocks: two blocks per frame
+    assert cap(ctypes.byref(_p(B, heads=1, frames=4, T=128)), B.head_table([(1, 0)])) == 2
+    # one 300-token frame: every block shares it
+    assert cap(ctypes.byref(_p(B, heads=1, frames=1, T=300)), B.head_table([(1, 0)])) == 5
+
+
+def test_calls_reject_bad_arguments_before_launch(B):
+    lib = B.load()
+    p = _p(B, heads=2, frames=2, T=100)
+    t = B.head_table([(1, 0), (2, 2)])
+    fake = ctypes.c_void_p(0x1000)  # never dereferenced: validation fails first
+    assert lib.saf3r_estimate_blocks(ctypes.byref(p), t, None, fake, fake, fake, None) == -1
+    assert lib.saf3r_estimate_blocks(ctypes.byref(_p(B, head_dim=32)), t, fake, fake, fake, fake, None) == -2
+    assert lib.saf3r_select_blocks(ctypes.byref(p), t, fake, fake, fake, fake, 3, None, None) == -3
+    assert lib.saf3r_select_blocks(ctypes.byref(p), t, fake, None, fake, fake, 8, None, None) == -1
+    assert lib.saf3r_select_blocks(ctypes.byref(p), B.head_table([(1, 0), (2, 9)]),
+                                   fake, fake, fake, fake, 8, None, None) == -5
+    assert lib.saf3r_sparse_attention(ctypes.byref(p), t, fake, fake, fake, fake, fake, 4,
+                                      None, None, None) == -1
+    assert lib.saf3r_sparse_attention(ctypes.byref(p), t, fake, fake, fake, None, fake, 4,
+                                      fake, None, None) == -1
+    assert lib.saf3r_sparse_attention(ctypes.byref(p), t, fake, fake, fake, fake, fake, 1,
+                                      fake, None, None) == -3
+
+
+def test_status_strings(B):
+    lib = B.load()
+    for s in (0, -1, -2, -3, -4, -5, 42):
+        assert lib.saf3r_status_string(s)
+    assert lib.saf3r_status_string(-3).decode().startswith("index capacity")
