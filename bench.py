@@ -1,0 +1,304 @@
+"""Benchmark of the SAF3R global-attention hot path on one MI355X.
+
+A step is one pass of the whole path over one layer: block pooling
+(saf3r_estimate_blocks), selection (saf3r_select_blocks) and attention over
+the kept blocks (saf3r_sparse_attention), inputs resident in HBM. Default
+workload: 100 frames x 1374 tokens = 137400 tokens, 16 heads x 64, bf16,
+table with 6 frame-local and 10 Top-K heads (target block sparsity 95%).
+
+Prints one JSON line: dense-equivalent TFLOP/s (4 N^2 64 H per layer over
+the measured step time) with ms per step, the attention kernel's roofline,
+the estimation kernel's HBM rate, the dense baseline from the same kernel,
+and the CPU oracle timed on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "ms per global-attn layer + dense-equiv TFLOP/s at S=100×1374 tok, 16 heads"
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_F32_TFLOPS = 157.3     # MI355X fp32 matrix
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_traffic.json")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def kept_flops(idx, cnt, table, n, nb):
+    """Algorithmic attention FLOP: sum over kept (query block, key block)
+    pairs of 4 * n_i * n_j * 64, counting valid tokens only."""
+    last = n - (nb - 1) * 64
+    rows = np.full(nb, 64, np.int64)
+    rows[-1] = last
+    total = 0
+    for h, (pattern, _) in enumerate(table):
+        if pattern == 0:
+            total += 4 * n * n * 64
+            continue
+        c = cnt[h].astype(np.int64)
+        listed = np.arange(idx.shape[2])[None, :] < c[:, None]
+        has_last = ((idx[h] == nb - 1) & listed).any(axis=1)
+        keys = 64 * c - (64 - last) * has_last
+        total += int(4 * 64 * np.sum(rows * keys))
+    return total
+
+
+def source_sha(path):
+    return hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
+
+
+def recorded_traffic(workload):
+    """HBM bytes per attention launch from the committed rocprofv3 counter
+    runs, if they were taken on the current kernel source."""
+    try:
+        rec = json.load(open(TRAFFIC_FILE))
+    except (OSError, ValueError):
+        return None
+    cur = source_sha(os.path.join(ROOT, "paper_2607_03612_amd", "csrc", "attn.hip"))
+    r = rec.get(workload)
+    if not r or r.get("attn_source_sha") != cur:
+        return None
+    return r.get("bytes_per_launch")
+
+
+def oracle_sample(w, q, k, v, table, rows_per_head, seed=0):
+    """The fp64 oracle on a seeded sample of query blocks of every head.
+
+    Per head, the full per-head work (widening to fp64, pooling every key
+    block of a Top-K head) is timed once; the per-query-block work (probe,
+    scores, selection, attention) is timed on the sample and scaled to all
+    query blocks. Returns (estimated seconds per layer, sampled rows per head)."""
+    import oracle as O
+
+    nb, n, T = w.nb, w.tokens, w.tokens_per_frame
+    rows = sorted(np.random.default_rng(seed).choice(nb, size=min(rows_per_head, nb), replace=False))
+    est = 0.0
+    for h, (pattern, topk) in enumerate(table):
+        t0 = time.perf_counter()
+        qh, kh, vh = (O.to_f64(x[h], w.dtype) for x in (q, k, v))
+        kbar = O.pool_blocks(kh, 64) if pattern == O.TOPK else None
+        t1 = time.perf_counter()
+        for i in rows:
+            r = O.block_range(i, n, 64)
+            if pattern == O.TOPK:
+                qbar = O.pool_blocks(qh[r.start:r.stop], 64)
+                lst, _ = O.topk_row(O.block_scores(qbar, kbar)[0], topk)
+            elif pattern == O.FRAME_LOCAL:
+                lst = O.frame_local_row(i, n, T, 64)
+            else:
+                lst = np.arange(nb)
+            O.attend_block(qh, kh, vh, i, lst, 64)
+        t2 = time.perf_counter()
+        est += (t1 - t0) + (t2 - t1) * nb / len(rows)
+    return est, len(rows)
+
+
+def blas_threads():
+    try:
+        import threadpoolctl
+
+        info = threadpoolctl.threadpool_info()
+        n = max((p.get("num_threads", 1) for p in info if p.get("user_api") == "blas"), default=1)
+        return int(n)
+    except Exception:
+        return os.cpu_count() or 1
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="S100xT1374-bf16")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--dense-reps", type=int, default=3)
+    ap.add_argument("--cpu-rows", type=int, default=320,
+                    help="query blocks per head in the oracle CPU sample (0 = skip)")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
+              "(the heads of a layer would shard across GPUs with no exchange)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2607_03612_amd as P
+    from paper_2607_03612_amd import binding
+    from workloads import WORKLOADS, make_qkv, make_table
+
+    if not os.path.exists(binding.LIB_PATH):
+        from paper_2607_03612_amd import build
+
+        build.build()
+    P.load()
+    if not torch.cuda.is_available():
+        raise SystemExit("no GPU visible: the HIP path needs an MI355X")
+
+    w = WORKLOADS[args.workload]
+    t0 = time.time()
+    q, k, v = make_qkv(w, seed=args.seed)
+    table = make_table(w, seed=args.seed)
+    log(f"[bench] {w.name}: N={w.tokens} nb={w.nb} table={table} (gen {time.time() - t0:.1f}s)")
+    code = P.BF16 if w.dtype == "bf16" else P.F32
+
+    def up(x):
+        if w.dtype == "bf16":
+            return torch.from_numpy(x.view(np.int16)).cuda().view(torch.bfloat16)
+        return torch.from_numpy(x).cuda()
+
+    tq, tk, tv = up(q), up(k), up(v)
+    H, N, nb, S, T = w.heads, w.tokens, w.nb, w.frames, w.tokens_per_frame
+    dev = tq.device
+    cap = P.index_capacity(table, S, T, code)
+    qp = torch.zeros((H, nb, 64), dtype=torch.float64, device=dev)
+    kp = torch.zeros_like(qp)
+    idx = torch.empty((H, nb, cap), dtype=torch.int32, device=dev)
+    cnt = torch.empty((H, nb), dtype=torch.int32, device=dev)
+    out = torch.empty_like(tq)
+
+    def step(ev=None):
+        if ev:
+            ev[0].record()
+        P.estimate_blocks(tq, tk, table, S, T, qp, kp)
+        if ev:
+            ev[1].record()
+        P.select_blocks(qp, kp, table, S, T, cap, idx, cnt, dtype=code)
+        if ev:
+            ev[2].record()
+        P.sparse_attention(tq, tk, tv, table, S, T, idx, cnt, out)
+        if ev:
+            ev[3].record()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for s in range(args.steps):
+        step(evs[s])
+    end.record()
+    torch.cuda.synchronize()
+    ms_step = start.elapsed_time(end) / args.steps
+    est_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
+    sel_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
+    att_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
+
+    idx_h, cnt_h = idx.cpu().numpy(), cnt.cpu().numpy()
+    flops_kept = kept_flops(idx_h, cnt_h, table, N, nb)
+    flops_dense = 4 * N * N * 64 * H
+    kept_pairs = sum(nb * nb if p == 0 else int(cnt_h[h].sum()) for h, (p, _) in enumerate(table))
+    sparsity = 1.0 - kept_pairs / (H * nb * nb)
+    esz = 2 if w.dtype == "bf16" else 4
+    n_topk = sum(1 for p, _ in table if p == 2)
+    est_bytes = 2 * n_topk * N * 64 * esz + 2 * n_topk * nb * 64 * 8
+    peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
+    att_tflops = flops_kept / (att_ms * 1e-3) / 1e12
+    value = flops_dense / (ms_step * 1e-3) / 1e12
+    log(f"[bench] step {ms_step:.3f} ms (estimate {est_ms:.3f}, select {sel_ms:.3f}, "
+        f"attention {att_ms:.3f}); sparsity {sparsity:.4f}; attention {att_tflops:.1f} TFLOP/s")
+
+    # dense baseline: the same attention kernel with every head dense
+    dense_tab = [(0, 0)] * H
+    dense = None
+    if args.dense_reps > 0:
+        P.sparse_attention(tq, tk, tv, dense_tab, S, T, out=out)
+        torch.cuda.synchronize()
+        d0, d1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        d0.record()
+        for _ in range(args.dense_reps):
+            P.sparse_attention(tq, tk, tv, dense_tab, S, T, out=out)
+        d1.record()
+        torch.cuda.synchronize()
+        dense_ms = d0.elapsed_time(d1) / args.dense_reps
+        dense = {"ms": round(dense_ms, 3),
+                 "tflops": round(flops_dense / (dense_ms * 1e-3) / 1e12, 1),
+                 "mfma_frac": round(flops_dense / (dense_ms * 1e-3) / 1e12 / peak, 4),
+                 "sparse_step_speedup": round(dense_ms / ms_step, 2)}
+        log(f"[bench] dense baseline {dense}")
+
+    # estimation kernel alone with a cold last-level cache (512 MiB scribble)
+    scribble = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+    e_ms = []
+    for _ in range(5):
+        scribble.fill_(1)
+        a0, a1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a0.record()
+        P.estimate_blocks(tq, tk, table, S, T, qp, kp)
+        a1.record()
+        torch.cuda.synchronize()
+        e_ms.append(a0.elapsed_time(a1))
+    est_cold_ms = float(np.median(e_ms))
+    del scribble
+
+    cpu = None
+    if args.cpu_rows > 0:
+        t0 = time.perf_counter()
+        sec, rows = oracle_sample(w, q, k, v, table, args.cpu_rows, seed=args.seed)
+        wall = time.perf_counter() - t0
+        cpu = {"value": round(flops_dense / sec / 1e12, 6), "unit": "dense-equiv TFLOP/s",
+               "cores": blas_threads(), "kind": "oracle",
+               "ms_per_layer": round(sec * 1e3, 1),
+               "sample": f"{rows} of {nb} query blocks per head (seeded), all 16 heads; per-head "
+                         f"fp64 widening and key pooling timed in full, per-block probe/score/"
+                         f"select/attention scaled by {nb}/{rows}; {wall:.1f} s of CPU work"}
+        log(f"[bench] cpu oracle {cpu}")
+
+    traffic = recorded_traffic(w.name)
+    result = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "dense-equiv TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {
+            "workload": w.name, "frames": S, "tokens_per_frame": T, "tokens": N, "heads": H,
+            "head_dim": 64, "block": 64, "key_blocks": nb,
+            "table": {"dense": sum(p == 0 for p, _ in table), "frame_local": sum(p == 1 for p, _ in table),
+                      "topk": n_topk, "topk_blocks": sorted({t for p, t in table if p == 2})},
+            "achieved_block_sparsity": round(sparsity, 4),
+        },
+        "roofline": {
+            "kernel": "attn_bf16_kernel" if w.dtype == "bf16" else "attn_f32_kernel",
+            "bound": "mfma", "achieved": round(att_tflops, 2), "peak": peak, "unit": "TFLOP/s",
+            "frac": round(att_tflops / peak, 4), "traffic": traffic,
+            "flop_per_launch": flops_kept, "launch_ms": round(att_ms, 4),
+        },
+        "kernels_ms": {"estimate": round(est_ms, 4), "select": round(sel_ms, 4),
+                       "attention": round(att_ms, 4)},
+        "estimate_roofline": {
+            "kernel": "pool_bf16_kernel" if w.dtype == "bf16" else "pool_f32_kernel",
+            "bound": "hbm", "bytes_per_launch": est_bytes, "launch_ms_cold": round(est_cold_ms, 4),
+            "achieved": round(est_bytes / (est_cold_ms * 1e-3) / 1e9, 1), "peak": PEAK_HBM_GBS,
+            "unit": "GB/s", "frac": round(est_bytes / (est_cold_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+        },
+        "dense_baseline": dense,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()
