@@ -164,7 +164,7 @@ def main():
     dev = tq.device
     cap = P.index_capacity(table, S, T, code)
     qp = torch.zeros((H, nb, 64), dtype=torch.float64, device=dev)
-    kp = torch.zeros_like(qp)
+    kp = torch.zeros((H, 64, nb), dtype=torch.float64, device=dev)
     idx = torch.empty((H, nb, cap), dtype=torch.int32, device=dev)
     cnt = torch.empty((H, nb), dtype=torch.int32, device=dev)
     out = torch.empty_like(tq)

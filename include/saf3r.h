@@ -85,13 +85,15 @@ int32_t saf3r_num_blocks(const saf3r_problem* problem);
 int32_t saf3r_index_capacity(const saf3r_problem* problem, const saf3r_head_cfg* table);
 
 /* Block pooling (Sec. 4.3: the probe of a set of queries is their mean).
- * For every TOPK head h and block b:
- *   q_pooled[h][b][:] = mean of Q[h][t][:] over the tokens t of block b
- *   k_pooled[h][b][:] = mean of K[h][t][:] likewise
+ * For every TOPK head h, block b and dimension d:
+ *   q_pooled[h][b][d] = mean of Q[h][t][d] over the tokens t of block b
+ *   k_pooled[h][d][b] = mean of K[h][t][d] likewise (dimension-major, so
+ *                       that the scoring pass reads it coalesced)
  * in float64 (a partial last block is divided by its own token count).
- *   q, k               device, [heads, N, 64] of problem->dtype
- *   q_pooled, k_pooled device, float64 [heads, nb, 64]; rows of non-TOPK
- *                      heads are left untouched
+ *   q, k      device, [heads, N, 64] of problem->dtype
+ *   q_pooled  device, float64 [heads, nb, 64]
+ *   k_pooled  device, float64 [heads, 64, nb]
+ *   Entries of non-TOPK heads are left untouched.
  * Returns SAF3R_OK, or an error with nothing enqueued. */
 saf3r_status saf3r_estimate_blocks(const saf3r_problem* problem, const saf3r_head_cfg* table,
                                    const void* q, const void* k,
@@ -106,8 +108,8 @@ saf3r_status saf3r_estimate_blocks(const saf3r_problem* problem, const saf3r_hea
  *   TOPK:         the topk_blocks highest scores s[i][j] = qbar_i . kbar_j / 8
  *                 (computed in float64), ties to the lower j.
  * Lists are written ascending, padded with -1 up to cap.
- *   q_pooled, k_pooled device float64 [heads, nb, 64] from saf3r_estimate_blocks
- *                      (read for TOPK heads only)
+ *   q_pooled, k_pooled device float64, [heads, nb, 64] and [heads, 64, nb], as
+ *                      written by saf3r_estimate_blocks (read for TOPK heads only)
  *   block_idx          device int32 [heads, nb, cap]
  *   block_cnt          device int32 [heads, nb]
  *   cap                >= saf3r_index_capacity(problem, table)
@@ -127,7 +129,8 @@ saf3r_status saf3r_select_blocks(const saf3r_problem* problem, const saf3r_head_
  *   out[t] = sum_u softmax(z)_u v_u
  *   lse[t] = log(sum_u exp(z_u))            (natural log)
  * bf16 inputs: Q K^T and P V on bf16 matrix cores with fp32 accumulation, the
- * softmax in fp32, P rounded to bf16 for P V, out rounded to bf16. fp32
+ * softmax in fp32, P rounded to bf16 for P V and for the row sum that
+ * normalises out and gives lse, out rounded to bf16. fp32
  * inputs: everything in fp32.
  *   q, k, v      device [heads, N, 64] of problem->dtype
  *   block_idx, block_cnt, cap   as written by saf3r_select_blocks; entries of

@@ -144,7 +144,8 @@ def index_capacity(table, frames, tokens_per_frame, dtype=BF16) -> int:
 
 def estimate_blocks(q, k, table, frames, tokens_per_frame, q_pooled=None, k_pooled=None,
                     stream=None):
-    """Pooled Q and K (float64 ``[heads, nb, 64]``; Top-K heads only)."""
+    """Pooled Q ``[heads, nb, 64]`` and pooled K ``[heads, 64, nb]`` (float64;
+    Top-K heads only)."""
     import torch
 
     _check_qkv(q, k)
@@ -155,7 +156,7 @@ def estimate_blocks(q, k, table, frames, tokens_per_frame, q_pooled=None, k_pool
     if q_pooled is None:
         q_pooled = torch.zeros((H, nb, HEAD_DIM), dtype=torch.float64, device=q.device)
     if k_pooled is None:
-        k_pooled = torch.zeros((H, nb, HEAD_DIM), dtype=torch.float64, device=q.device)
+        k_pooled = torch.zeros((H, HEAD_DIM, nb), dtype=torch.float64, device=q.device)
     p = problem(H, frames, tokens_per_frame, _torch_dtype_code(q))
     _check(_lib().saf3r_estimate_blocks(ctypes.byref(p), head_table(table), _ptr(q), _ptr(k),
                                         _ptr(q_pooled), _ptr(k_pooled), _stream(stream)),
@@ -169,9 +170,10 @@ def select_blocks(q_pooled, k_pooled, table, frames, tokens_per_frame, cap=None,
     import torch
 
     H, nb, _ = q_pooled.shape
-    for t in (q_pooled, k_pooled):
-        if not (t.is_cuda and t.is_contiguous() and t.dtype == torch.float64 and t.shape == (H, nb, HEAD_DIM)):
-            raise ValueError("pooled tensors must be contiguous float64 [heads, nb, 64] on the device")
+    for t, shape in ((q_pooled, (H, nb, HEAD_DIM)), (k_pooled, (H, HEAD_DIM, nb))):
+        if not (t.is_cuda and t.is_contiguous() and t.dtype == torch.float64 and t.shape == shape):
+            raise ValueError("pooled tensors must be contiguous float64 device tensors, "
+                             "q [heads, nb, 64] and k [heads, 64, nb]")
     if cap is None:
         cap = index_capacity(table, frames, tokens_per_frame, dtype)
     dev = q_pooled.device

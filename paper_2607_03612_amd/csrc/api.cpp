@@ -157,14 +157,14 @@ saf3r_status saf3r_select_blocks(const saf3r_problem* problem, const saf3r_head_
       sa.pattern[sa.n_heads++] = (int8_t)table[h].pattern;
     }
   }
-  // Rows scored per workgroup: as many as fit while two workgroups share a
-  // CU's 160 KB of LDS, else as many as fit at all.
-  constexpr size_t kLdsPerCu = 160 * 1024;
-  int rows = 8;
-  while (rows > 1 && saf3r::topk_lds_bytes(rows, s.nb) > kLdsPerCu / 2) rows /= 2;
+  // Query blocks scored per workgroup: the most (up to 16) whose score rows
+  // fit in LDS; each key-block read is then shared by that many rows.
+  constexpr size_t kLdsBudget = 150 * 1024;
+  int rows = 16;
+  while (rows > 1 && saf3r::topk_lds_bytes(rows, s.nb) > kLdsBudget) rows /= 2;
   ta.rows_per_group = rows;
   const size_t lds = saf3r::topk_lds_bytes(rows, s.nb);
-  if (lds > kLdsPerCu) return SAF3R_ERR_UNSUPPORTED;
+  if (lds > kLdsBudget) return SAF3R_ERR_UNSUPPORTED;
 
   hipStream_t hs = static_cast<hipStream_t>(stream);
   hipError_t e = saf3r::launch_select_static(block_idx, block_cnt, sa, hs);

@@ -34,7 +34,6 @@ typedef int i32x2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 
 constexpr uint32_t kRsrcWord3 = 0x00020000u;  // gfx9 buffer descriptor: 32-bit raw data
-constexpr int kVStride = 72;                   // bf16 per LDS row of V: 64 + 8 pad
 constexpr int kFStride = 65;                   // fp32 per LDS row (fp32 path)
 constexpr float kNegInf = -__builtin_inff();
 constexpr float kLn2 = 0.6931471805599453f;
@@ -69,26 +68,63 @@ __device__ inline Work work_item(const AttnArgs& a) {
 
 // ------------------------------------------------------------------ bf16
 
-// K tile j as the A operand of v_mfma_f32_32x32x16_bf16: rows = keys.
-// kA[tk][s]: key 64j + 32tk + (lane % 32), head dims 16s + 8(lane / 32) + [0, 8).
-__device__ inline void load_k_tile(bf16x8 (&kA)[2][4], __amdgpu_buffer_rsrc_t rk, int j,
-                                   int l32, int hf) {
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(3))) char lds_char;
+typedef __attribute__((address_space(3))) const bf16x8 lds_bf16x8;
+
+// LDS tiles: 64 rows x 128 B, 16-byte chunk c of row r stored at slot
+// c ^ (r & 7). Reads of 8 rows at one chunk (MFMA operands) and the
+// transposing reads (8 rows x 4 chunks) then spread over all banks.
+__device__ inline int swz(int r, int c) { return r * 128 + ((c ^ (r & 7)) << 4); }
+
+// One 64x64 bf16 tile (rows 64j.. of the head) into LDS with the direct
+// buffer-to-LDS load: instruction n fills LDS bytes [1024n, 1024n + 1024),
+// lane l its 16 bytes at 16l, i.e. row 8n + l/8, slot l%8, which must hold
+// chunk (l%8) ^ (l/8). Rows past the head read as zeros.
+// `lane_off` is the lane's byte offset inside an 8-row group,
+// ((l/8) * 64 + ((l%8) ^ (l/8)) * 8) * 2; the tile and group offsets are
+// wave-uniform and go in the scalar offset.
+__device__ inline int dma_lane_offset(int lane) {
+  return ((lane >> 3) * kHeadDim + (((lane & 7) ^ (lane >> 3)) * 8)) * 2;
+}
+__device__ inline void dma_tile(__amdgpu_buffer_rsrc_t r, int j, lds_char* tile, int lane_off) {
+  const int base = __builtin_amdgcn_readfirstlane(j * kBlock * kHeadDim * 2);  // j is wave-uniform
 #pragma unroll
-  for (int tk = 0; tk < 2; ++tk)
-#pragma unroll
-    for (int s = 0; s < 4; ++s)
-      kA[tk][s] = load_b128(
-          rk, (uint32_t)(((j * kBlock + 32 * tk + l32) * kHeadDim + 16 * s + 8 * hf) * 2));
+  for (int n = 0; n < 8; ++n)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)(tile + 1024 * n), 16, lane_off,
+                                             base + n * 8 * kHeadDim * 2, 0, 0);
 }
 
-__global__ __launch_bounds__(64) void attn_bf16_kernel(const uint16_t* __restrict__ q,
+// The compiler does not track the direct-to-LDS loads: wait for them by hand.
+__device__ inline void wait_dma() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+__device__ inline void wait_lds() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+
+// max / sum of a value over the lane pair (l, l ^ 32) that shares a query
+__device__ inline float pair_max(float x) {
+  const auto s = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(s[0]), __uint_as_float(s[1]));
+}
+__device__ inline float pair_sum(float x) {
+  const auto s = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(s[0]) + __uint_as_float(s[1]);
+}
+
+// The running max is only raised when a tile's max exceeds it by more than
+// this (log2 units): P stays <= 2^8 and O is rescaled rarely.
+constexpr float kRescaleSlack = 8.0f;
+
+template <bool kAllDense>
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_bf16_kernel(const uint16_t* __restrict__ q,
                                                       const uint16_t* __restrict__ k,
                                                       const uint16_t* __restrict__ v,
                                                       const int32_t* __restrict__ idx,
                                                       const int32_t* __restrict__ cnt,
                                                       uint16_t* __restrict__ out,
                                                       float* __restrict__ lse, AttnArgs a) {
-  __shared__ __attribute__((aligned(16))) __bf16 vs[kBlock * kVStride];
+  // LDS pointers stay in address space 3 (no generic-pointer casts)
+  __shared__ __attribute__((aligned(1024))) char smem[2 * 64 * 128];
+  lds_char* const ks = (lds_char*)smem;
+  lds_char* const vs = ks + 64 * 128;
 
   const Work w = work_item(a);
   if (!w.valid) return;
@@ -96,7 +132,7 @@ __global__ __launch_bounds__(64) void attn_bf16_kernel(const uint16_t* __restric
   const int l32 = lane & 31;
   const int hf = lane >> 5;
   const int nb = a.nb;
-  const bool dense = a.dense[w.h] != 0;
+  const bool dense = kAllDense || a.dense[w.h] != 0;
   const int32_t* list = idx + ((int64_t)w.h * nb + w.i) * a.cap;
   int count = nb;
   if (!dense) count = min(max(cnt[(int64_t)w.h * nb + w.i], 0), a.cap);
@@ -107,6 +143,11 @@ __global__ __launch_bounds__(64) void attn_bf16_kernel(const uint16_t* __restric
   const __amdgpu_buffer_rsrc_t rk = make_rsrc(k + head_off, head_bytes);
   const __amdgpu_buffer_rsrc_t rv = make_rsrc(v + head_off, head_bytes);
   const __amdgpu_buffer_rsrc_t ro = make_rsrc(out + head_off, head_bytes);
+
+  const int dma_off = dma_lane_offset(lane);
+  int j = count > 0 ? (dense ? 0 : list[0]) : 0;
+  dma_tile(rk, j, ks, dma_off);
+  dma_tile(rv, j, vs, dma_off);
 
   // Q^T as the B operand: qB[tq][s] = Q[64i + 32tq + l32][16s + 8hf + (0..7)]
   bf16x8 qB[2][4];
@@ -129,40 +170,37 @@ __global__ __launch_bounds__(64) void attn_bf16_kernel(const uint16_t* __restric
 
   const bool tail = (a.n % kBlock) != 0;
   const float sc = a.scale_log2;
-
-  // transposing-read addresses (element offsets in vs) for V^T operands
+  // transposing-read position of this lane inside a 4-row x 16-column group
   const int tr_row = 4 * hf + ((lane & 15) >> 2);
   const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
 
-  bf16x8 kA[2][4];
-  int j = count > 0 ? (dense ? 0 : list[0]) : 0;
-  load_k_tile(kA, rk, j, l32, hf);
-
   for (int it = 0; it < count; ++it) {
-    // V tile j: rows 8n + lane/8, 16-byte chunk lane%8 (coalesced 1 KB per load)
-    i32x4 vreg[8];
-#pragma unroll
-    for (int n8 = 0; n8 < 8; ++n8)
-      vreg[n8] = __builtin_amdgcn_raw_buffer_load_b128(
-          rv, (int)(((j * kBlock + 8 * n8 + (lane >> 3)) * kHeadDim + (lane & 7) * 8) * 2), 0, 0);
+    const int jcur = j;
+    const bool more = it + 1 < count;
+    if (more) j = dense ? it + 1 : list[it + 1];
+    wait_dma();  // K and V of tile jcur are in LDS
 
-    // S^T[tk][tq] (keys 32tk.., queries 32tq..)
+    // S^T[tk][tq] = K Q^T (keys 32tk.., queries 32tq..); K rows as A operand
     f32x16 s[2][2];
 #pragma unroll
-    for (int tk = 0; tk < 2; ++tk)
+    for (int tk = 0; tk < 2; ++tk) {
+      bf16x8 kA[4];
+#pragma unroll
+      for (int st = 0; st < 4; ++st)
+        kA[st] = *(lds_bf16x8*)(ks + swz(32 * tk + l32, 2 * st + hf));
 #pragma unroll
       for (int tq = 0; tq < 2; ++tq) {
         f32x16 acc = {};
 #pragma unroll
         for (int st = 0; st < 4; ++st)
-          acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kA[tk][st], qB[tq][st], acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kA[st], qB[tq][st], acc, 0, 0, 0);
         s[tk][tq] = acc;
       }
-
-    const int jcur = j;
-    if (it + 1 < count) {
-      j = dense ? it + 1 : list[it + 1];
-      load_k_tile(kA, rk, j, l32, hf);
+    }
+    // the K operands are in registers: refill the K tile for the next step
+    if (more) {
+      wait_lds();
+      dma_tile(rk, j, ks, dma_off);
     }
 
     if (tail && jcur == nb - 1) {
@@ -179,66 +217,71 @@ __global__ __launch_bounds__(64) void attn_bf16_kernel(const uint16_t* __restric
         }
     }
 
-    // online softmax per query column (this lane and lane ^ 32 share it)
+    // online softmax per query column (lanes l and l ^ 32 share it). P is
+    // rounded to bf16 here, and the row sum adds the rounded values, so the
+    // normaliser matches the weights the P V product actually uses.
+    bf16x8 pB[2][2][2];  // [tk][u][tq]: keys 32tk + 16u.. as the B operand
 #pragma unroll
     for (int tq = 0; tq < 2; ++tq) {
-      float mx = s[0][tq][0];
+      float mx = fmaxf(s[0][tq][0], s[0][tq][1]);
 #pragma unroll
-      for (int e = 1; e < 16; ++e) mx = fmaxf(mx, s[0][tq][e]);
+      for (int e = 2; e < 16; e += 2) mx = fmaxf(mx, fmaxf(s[0][tq][e], s[0][tq][e + 1]));
 #pragma unroll
-      for (int e = 0; e < 16; ++e) mx = fmaxf(mx, s[1][tq][e]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float mnew = fmaxf(m[tq], mx * sc);
-      const float alpha = fast_exp2(m[tq] - mnew);
-      m[tq] = mnew;
+      for (int e = 0; e < 16; e += 2) mx = fmaxf(mx, fmaxf(s[1][tq][e], s[1][tq][e + 1]));
+      const float tile_max = pair_max(mx) * sc;
+      const float mnew = tile_max > m[tq] + kRescaleSlack ? tile_max : m[tq];
+      if (__ballot(mnew != m[tq])) {  // wave-uniform: rescale only when some max moved
+        const float alpha = fast_exp2(m[tq] - mnew);
+        m[tq] = mnew;
+        l[tq] *= alpha;
+#pragma unroll
+        for (int c = 0; c < 2; ++c) o[c][tq] *= alpha;
+      }
+      const float mcur = m[tq];
       float rs = 0.f;
 #pragma unroll
       for (int tk = 0; tk < 2; ++tk)
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const float p = fast_exp2(fmaf(s[tk][tq][e], sc, -mnew));
-          s[tk][tq][e] = p;
-          rs += p;
-        }
-      l[tq] = fmaf(l[tq], alpha, rs);
+        for (int u = 0; u < 2; ++u)
 #pragma unroll
-      for (int c = 0; c < 2; ++c) o[c][tq] *= alpha;
+          for (int e = 0; e < 8; ++e) {
+            const __bf16 pb = (__bf16)fast_exp2(fmaf(s[tk][tq][8 * u + e], sc, -mcur));
+            pB[tk][u][tq][e] = pb;
+            rs += (float)pb;
+          }
+      l[tq] += rs;
     }
-
-    // stage V in LDS (same wave wrote and reads it: no barrier needed)
-#pragma unroll
-    for (int n8 = 0; n8 < 8; ++n8)
-      *reinterpret_cast<i32x4*>(&vs[(8 * n8 + (lane >> 3)) * kVStride + (lane & 7) * 8]) = vreg[n8];
 
     // O^T[c][tq] += V^T[c][keys] P^T[keys][tq]
 #pragma unroll
     for (int tk = 0; tk < 2; ++tk)
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
-        bf16x8 pB[2];
-#pragma unroll
-        for (int tq = 0; tq < 2; ++tq)
-#pragma unroll
-          for (int e = 0; e < 8; ++e) pB[tq][e] = (__bf16)s[tk][tq][8 * u + e];
         const int krow = 32 * tk + 16 * u + tr_row;
 #pragma unroll
         for (int c = 0; c < 2; ++c) {
+          const int col = 32 * c + tr_col;
           const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
-              (lds_bf16x4*)(&vs[krow * kVStride + 32 * c + tr_col]));
+              (lds_bf16x4*)(vs + swz(krow, col >> 3) + (col & 7) * 2));
           const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
-              (lds_bf16x4*)(&vs[(krow + 8) * kVStride + 32 * c + tr_col]));
+              (lds_bf16x4*)(vs + swz(krow + 8, col >> 3) + (col & 7) * 2));
           const bf16x8 vA = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
 #pragma unroll
           for (int tq = 0; tq < 2; ++tq)
-            o[c][tq] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vA, pB[tq], o[c][tq], 0, 0, 0);
+            o[c][tq] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vA, pB[tk][u][tq], o[c][tq], 0, 0, 0);
         }
       }
+    // the V operands are consumed: refill the V tile for the next step
+    if (more) {
+      wait_lds();
+      dma_tile(rv, j, vs, dma_off);
+    }
   }
 
   // epilogue: normalise, round to bf16, store; log-sum-exp in natural log
 #pragma unroll
   for (int tq = 0; tq < 2; ++tq) {
-    const float lt = l[tq] + __shfl_xor(l[tq], 32);
+    const float lt = pair_sum(l[tq]);
     const float inv = 1.0f / lt;
     const int query = w.i * kBlock + 32 * tq + l32;
 #pragma unroll
@@ -430,8 +473,11 @@ hipError_t launch_attention(int dtype, const void* q, const void* k, const void*
                             const AttnArgs& a, hipStream_t s) {
   const int64_t groups = 8LL * a.heads * a.slab;
   if (groups == 0) return hipSuccess;
+  bool all_dense = true;
+  for (int h = 0; h < a.heads; ++h) all_dense = all_dense && a.dense[h];
   if (dtype == 1) {
-    hipLaunchKernelGGL(attn_bf16_kernel, dim3((unsigned)groups), dim3(64), 0, s,
+    auto kern = all_dense ? attn_bf16_kernel<true> : attn_bf16_kernel<false>;
+    hipLaunchKernelGGL(kern, dim3((unsigned)groups), dim3(64), 0, s,
                        static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
                        static_cast<const uint16_t*>(v), idx, cnt, static_cast<uint16_t*>(out),
                        lse, a);

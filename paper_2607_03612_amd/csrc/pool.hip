@@ -5,7 +5,9 @@
 // HBM-bound: each 64x64 tile is read once with 16-byte coalesced loads (one
 // wave per tile, eight rows of 128 B per load instruction) and summed in
 // float64, which is exact for bf16 inputs (8-bit significands summed in a
-// 53-bit significand), then divided by the block's own token count.
+// 53-bit significand), then divided by the block's own token count. Pooled Q
+// is written [H][nb][64]; pooled K dimension-major [H][64][nb], the layout
+// the scoring reads coalesce on.
 #include "saf3r_internal.h"
 
 namespace saf3r {
@@ -37,13 +39,17 @@ __global__ __launch_bounds__(256) void pool_bf16_kernel(const uint16_t* __restri
   const int r = lane >> 3;  // row within each group of 8 rows
   const int c = lane & 7;   // 16-byte chunk = 8 columns
 
+  // rows past a partial last block load a clamped valid row (so all eight
+  // loads issue back to back) and are zeroed afterwards
   uint4 v[8];
 #pragma unroll
   for (int it = 0; it < 8; ++it) {
     const int row = r + 8 * it;
-    v[it] = row < rows ? *reinterpret_cast<const uint4*>(src + row * kHeadDim + c * 8)
-                       : make_uint4(0, 0, 0, 0);
+    v[it] = *reinterpret_cast<const uint4*>(src + min(row, rows - 1) * kHeadDim + c * 8);
   }
+#pragma unroll
+  for (int it = 0; it < 8; ++it)
+    if (r + 8 * it >= rows) v[it] = make_uint4(0, 0, 0, 0);
   double acc[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) acc[e] = 0.0;
@@ -63,14 +69,20 @@ __global__ __launch_bounds__(256) void pool_bf16_kernel(const uint16_t* __restri
     for (int e = 0; e < 8; ++e) acc[e] += __shfl_xor(acc[e], m);
   }
   if (r == 0) {
-    double* dst = (tensor ? kp : qp) + ((int64_t)h * a.nb + b) * kHeadDim + c * 8;
-    const double inv_rows = (double)rows;
+    const double nrows = (double)rows;
+    if (tensor == 0) {
+      double* dst = qp + ((int64_t)h * a.nb + b) * kHeadDim + c * 8;
 #pragma unroll
-    for (int e = 0; e < 8; e += 2) {
-      double2 o;
-      o.x = acc[e] / inv_rows;
-      o.y = acc[e + 1] / inv_rows;
-      *reinterpret_cast<double2*>(dst + e) = o;
+      for (int e = 0; e < 8; e += 2) {
+        double2 o;
+        o.x = acc[e] / nrows;
+        o.y = acc[e + 1] / nrows;
+        *reinterpret_cast<double2*>(dst + e) = o;
+      }
+    } else {  // dimension-major [H][64][nb]
+      double* dst = kp + ((int64_t)h * kHeadDim + c * 8) * a.nb + b;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) dst[(int64_t)e * a.nb] = acc[e] / nrows;
     }
   }
 }
@@ -96,16 +108,15 @@ __global__ __launch_bounds__(256) void pool_f32_kernel(const float* __restrict__
   const int c = lane & 15;  // 16-byte chunk = 4 columns
 
   double acc[4] = {0.0, 0.0, 0.0, 0.0};
-#pragma unroll 4
+#pragma unroll
   for (int it = 0; it < 16; ++it) {
     const int row = r + 4 * it;
-    if (row < rows) {
-      const float4 x = *reinterpret_cast<const float4*>(src + row * kHeadDim + c * 4);
-      acc[0] += (double)x.x;
-      acc[1] += (double)x.y;
-      acc[2] += (double)x.z;
-      acc[3] += (double)x.w;
-    }
+    float4 x = *reinterpret_cast<const float4*>(src + min(row, rows - 1) * kHeadDim + c * 4);
+    if (row >= rows) x = make_float4(0.f, 0.f, 0.f, 0.f);
+    acc[0] += (double)x.x;
+    acc[1] += (double)x.y;
+    acc[2] += (double)x.z;
+    acc[3] += (double)x.w;
   }
 #pragma unroll
   for (int m = 16; m < 64; m <<= 1) {
@@ -113,15 +124,21 @@ __global__ __launch_bounds__(256) void pool_f32_kernel(const float* __restrict__
     for (int e = 0; e < 4; ++e) acc[e] += __shfl_xor(acc[e], m);
   }
   if (r == 0) {
-    double* dst = (tensor ? kp : qp) + ((int64_t)h * a.nb + b) * kHeadDim + c * 4;
     const double nrows = (double)rows;
-    double2 o0, o1;
-    o0.x = acc[0] / nrows;
-    o0.y = acc[1] / nrows;
-    o1.x = acc[2] / nrows;
-    o1.y = acc[3] / nrows;
-    *reinterpret_cast<double2*>(dst) = o0;
-    *reinterpret_cast<double2*>(dst + 2) = o1;
+    if (tensor == 0) {
+      double* dst = qp + ((int64_t)h * a.nb + b) * kHeadDim + c * 4;
+      double2 o0, o1;
+      o0.x = acc[0] / nrows;
+      o0.y = acc[1] / nrows;
+      o1.x = acc[2] / nrows;
+      o1.y = acc[3] / nrows;
+      *reinterpret_cast<double2*>(dst) = o0;
+      *reinterpret_cast<double2*>(dst + 2) = o1;
+    } else {  // dimension-major [H][64][nb]
+      double* dst = kp + ((int64_t)h * kHeadDim + c * 4) * a.nb + b;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) dst[(int64_t)e * a.nb] = acc[e] / nrows;
+    }
   }
 }
 

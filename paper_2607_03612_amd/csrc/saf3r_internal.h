@@ -55,7 +55,7 @@ struct AttnArgs {
 
 hipError_t launch_pool(int dtype, const void* q, const void* k, double* qp, double* kp,
                        const PoolArgs& a, hipStream_t s);
-hipError_t launch_select_topk(const double* qp, const double* kp, int32_t* idx, int32_t* cnt,
+hipError_t launch_select_topk(const double* qp, const double* kpT, int32_t* idx, int32_t* cnt,
                               double* scores, const TopKArgs& a, size_t lds_bytes, hipStream_t s);
 hipError_t launch_select_static(int32_t* idx, int32_t* cnt, const StaticArgs& a, hipStream_t s);
 hipError_t launch_attention(int dtype, const void* q, const void* k, const void* v,
@@ -64,5 +64,7 @@ hipError_t launch_attention(int dtype, const void* q, const void* k, const void*
 
 // Bytes of LDS the Top-K selection kernel needs for `rows` query blocks.
 size_t topk_lds_bytes(int rows, int nb);
+// Threads per workgroup of the Top-K selection kernel for `rows` query blocks.
+int topk_threads(int rows);
 
 }  // namespace saf3r

@@ -9,8 +9,10 @@ TOL_BF16 = 2e-2          # max-abs error of bf16 outputs against the fp64 oracle
 TOL_F32 = 1e-4           # max-abs error of fp32 outputs against the fp64 oracle
 # Log-sum-exp: both dtypes accumulate the 64 products of q.k in fp32 (unit
 # roundoff 6e-8); with |q||k| up to ~200 on these inputs the score error is
-# ~1e-5 typical and bounded by ~1e-4, which the log-sum-exp inherits.
-LSE_TOL_BF16 = 2e-3
+# ~1e-5 typical and bounded by ~1e-4, which the log-sum-exp inherits. The bf16
+# path normalises by the sum of the bf16-rounded P it multiplies V with, so
+# its log-sum-exp also carries bf16's relative rounding of P (at most 2^-8).
+LSE_TOL_BF16 = 2.0 ** -8 + 1e-4
 LSE_TOL_F32 = 1e-4
 
 
@@ -42,7 +44,7 @@ def gpu_layer(P, w, q, k, v, table, want_scores=False, want_lse=True):
                                   want_lse=want_lse)
     torch.cuda.synchronize()
     res = {
-        "q_pooled": qp.cpu().numpy(), "k_pooled": kp.cpu().numpy(),
+        "q_pooled": qp.cpu().numpy(), "k_pooled": kp.transpose(1, 2).cpu().numpy(),
         "idx": idx.cpu().numpy(), "cnt": cnt.cpu().numpy(),
         "out": out_to_numpy(out), "lse": None if lse is None else lse.cpu().numpy().astype(np.float64),
         "scores": None if scores is None else scores.cpu().numpy(),
