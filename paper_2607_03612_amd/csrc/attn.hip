@@ -20,6 +20,8 @@
 // Launch order: workgroup b runs on XCD b % 8; each XCD takes a contiguous
 // slab of query blocks of every head (neighbouring query blocks share kept
 // key blocks, which then hit in that XCD's L2), heads in decreasing cost.
+#include <type_traits>
+
 #include "saf3r_internal.h"
 
 namespace saf3r {
@@ -27,6 +29,8 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef int i32x4 __attribute__((ext_vector_type(4)));
@@ -112,6 +116,7 @@ __device__ inline float pair_sum(float x) {
 // The running max is only raised when a tile's max exceeds it by more than
 // this (log2 units): P stays <= 2^8 and O is rescaled rarely.
 constexpr float kRescaleSlack = 8.0f;
+constexpr bf16x2 kOnes = {(__bf16)1.0f, (__bf16)1.0f};
 
 template <bool kAllDense>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_bf16_kernel(const uint16_t* __restrict__ q,
@@ -174,7 +179,10 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
   const int tr_row = 4 * hf + ((lane & 15) >> 2);
   const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
 
-  for (int it = 0; it < count; ++it) {
+  // One step of the online softmax over kept tile `it`. Only the last step
+  // can meet the partial last key block (lists are ascending), so only the
+  // peeled last step carries the key mask.
+  auto step = [&](int it, auto masked) {
     const int jcur = j;
     const bool more = it + 1 < count;
     if (more) j = dense ? it + 1 : list[it + 1];
@@ -203,31 +211,36 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
       dma_tile(rk, j, ks, dma_off);
     }
 
-    if (tail && jcur == nb - 1) {
-      const int valid_keys = (int)(a.n - (int64_t)jcur * kBlock);
+    if constexpr (decltype(masked)::value) {
+      if (tail && jcur == nb - 1) {
+        const int valid_keys = (int)(a.n - (int64_t)jcur * kBlock);
 #pragma unroll
-      for (int tk = 0; tk < 2; ++tk)
+        for (int tk = 0; tk < 2; ++tk)
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int key = 32 * tk + 8 * (e >> 2) + 4 * hf + (e & 3);
-          if (key >= valid_keys) {
-            s[tk][0][e] = kNegInf;
-            s[tk][1][e] = kNegInf;
+          for (int e = 0; e < 16; ++e) {
+            const int key = 32 * tk + 8 * (e >> 2) + 4 * hf + (e & 3);
+            if (key >= valid_keys) {
+              s[tk][0][e] = kNegInf;
+              s[tk][1][e] = kNegInf;
+            }
           }
-        }
+      }
     }
 
     // online softmax per query column (lanes l and l ^ 32 share it). P is
-    // rounded to bf16 here, and the row sum adds the rounded values, so the
-    // normaliser matches the weights the P V product actually uses.
+    // rounded to bf16 here, and the row sum adds the rounded values (one
+    // bf16 dot with (1, 1) per pair), so the normaliser matches the weights
+    // the P V product actually uses.
     bf16x8 pB[2][2][2];  // [tk][u][tq]: keys 32tk + 16u.. as the B operand
 #pragma unroll
     for (int tq = 0; tq < 2; ++tq) {
-      float mx = fmaxf(s[0][tq][0], s[0][tq][1]);
+      float mx = fmaxf(fmaxf(s[0][tq][0], s[0][tq][1]), s[0][tq][2]);
 #pragma unroll
-      for (int e = 2; e < 16; e += 2) mx = fmaxf(mx, fmaxf(s[0][tq][e], s[0][tq][e + 1]));
+      for (int e = 3; e < 15; e += 2) mx = fmaxf(fmaxf(mx, s[0][tq][e]), s[0][tq][e + 1]);
+      mx = fmaxf(fmaxf(mx, s[0][tq][15]), s[1][tq][0]);
 #pragma unroll
-      for (int e = 0; e < 16; e += 2) mx = fmaxf(mx, fmaxf(s[1][tq][e], s[1][tq][e + 1]));
+      for (int e = 1; e < 15; e += 2) mx = fmaxf(fmaxf(mx, s[1][tq][e]), s[1][tq][e + 1]);
+      mx = fmaxf(mx, s[1][tq][15]);
       const float tile_max = pair_max(mx) * sc;
       const float mnew = tile_max > m[tq] + kRescaleSlack ? tile_max : m[tq];
       if (__ballot(mnew != m[tq])) {  // wave-uniform: rescale only when some max moved
@@ -242,13 +255,18 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
 #pragma unroll
       for (int tk = 0; tk < 2; ++tk)
 #pragma unroll
-        for (int u = 0; u < 2; ++u)
+        for (int u = 0; u < 2; ++u) {
+          bf16x2 pr[4];
 #pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            const __bf16 pb = (__bf16)fast_exp2(fmaf(s[tk][tq][8 * u + e], sc, -mcur));
-            pB[tk][u][tq][e] = pb;
-            rs += (float)pb;
+          for (int e = 0; e < 4; ++e) {
+            const f32x2 pf = {fast_exp2(fmaf(s[tk][tq][8 * u + 2 * e], sc, -mcur)),
+                              fast_exp2(fmaf(s[tk][tq][8 * u + 2 * e + 1], sc, -mcur))};
+            pr[e] = __builtin_convertvector(pf, bf16x2);
+            rs = __builtin_amdgcn_fdot2_f32_bf16(pr[e], kOnes, rs, false);
           }
+          pB[tk][u][tq] = bf16x8{pr[0][0], pr[0][1], pr[1][0], pr[1][1],
+                                 pr[2][0], pr[2][1], pr[3][0], pr[3][1]};
+        }
       l[tq] += rs;
     }
 
@@ -276,7 +294,9 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
       wait_lds();
       dma_tile(rv, j, vs, dma_off);
     }
-  }
+  };
+  for (int it = 0; it + 1 < count; ++it) step(it, std::false_type{});
+  if (count > 0) step(count - 1, std::true_type{});
 
   // epilogue: normalise, round to bf16, store; log-sum-exp in natural log
 #pragma unroll
