@@ -76,32 +76,48 @@ typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(3))) char lds_char;
 typedef __attribute__((address_space(3))) const bf16x8 lds_bf16x8;
 
-// LDS tiles: 64 rows x 128 B, 16-byte chunk c of row r stored at slot
-// c ^ (r & 7). Reads of 8 rows at one chunk (MFMA operands) and the
-// transposing reads (8 rows x 4 chunks) then spread over all banks.
-__device__ inline int swz(int r, int c) { return r * 128 + ((c ^ (r & 7)) << 4); }
+// LDS tiles: 64 rows x 128 B; 16-byte chunk c of row r is stored at slot
+// c ^ f(r), f(r) = (bit2(r), bit1(r), bit0(r) ^ bit1(r) ^ bit3(r)). With it
+// the MFMA operand reads (16 rows at one chunk) and the transposing reads
+// (4 rows x 2 chunks per 16 lanes, 4 x 4 per 32) touch every bank once,
+// whether the LDS serves 128 or 256 bytes per clock.
+__device__ inline int swz_f(int r) {
+  return ((r >> 2) & 1) | (r & 2) | (((r ^ (r >> 1) ^ (r >> 3)) & 1) << 2);
+}
+__device__ inline int swz(int r, int c) { return r * 128 + ((c ^ swz_f(r)) << 4); }
 
 // One 64x64 bf16 tile (rows 64j.. of the head) into LDS with the direct
 // buffer-to-LDS load: instruction n fills LDS bytes [1024n, 1024n + 1024),
 // lane l its 16 bytes at 16l, i.e. row 8n + l/8, slot l%8, which must hold
-// chunk (l%8) ^ (l/8). Rows past the head read as zeros.
-// `lane_off` is the lane's byte offset inside an 8-row group,
-// ((l/8) * 64 + ((l%8) ^ (l/8)) * 8) * 2; the tile and group offsets are
+// chunk (l%8) ^ f(8n + l/8) = (l%8) ^ f(l/8) ^ (4 if n is odd). Rows past
+// the head read as zeros. The lane's byte offset inside its 8-row group
+// depends only on the parity of n; the tile and group offsets are
 // wave-uniform and go in the scalar offset.
-__device__ inline int dma_lane_offset(int lane) {
-  return ((lane >> 3) * kHeadDim + (((lane & 7) ^ (lane >> 3)) * 8)) * 2;
+struct DmaLaneOffsets {
+  int even, odd;
+};
+__device__ inline DmaLaneOffsets dma_lane_offset(int lane) {
+  const int r = lane >> 3;
+  const int c = (lane & 7) ^ swz_f(r);
+  return {(r * kHeadDim + c * 8) * 2, (r * kHeadDim + (c ^ 4) * 8) * 2};
 }
-__device__ inline void dma_tile(__amdgpu_buffer_rsrc_t r, int j, lds_char* tile, int lane_off) {
+__device__ inline void dma_tile(__amdgpu_buffer_rsrc_t r, int j, lds_char* tile,
+                                DmaLaneOffsets off) {
   const int base = __builtin_amdgcn_readfirstlane(j * kBlock * kHeadDim * 2);  // j is wave-uniform
 #pragma unroll
   for (int n = 0; n < 8; ++n)
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)(tile + 1024 * n), 16, lane_off,
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)(tile + 1024 * n), 16,
+                                             (n & 1) ? off.odd : off.even,
                                              base + n * 8 * kHeadDim * 2, 0, 0);
 }
 
-// The compiler does not track the direct-to-LDS loads: wait for them by hand.
-__device__ inline void wait_dma() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+// Waits on the direct-to-LDS loads. Vector memory loads complete in issue
+// order, and each tile is eight loads, so "all but the last eight" means "all
+// but the tile issued last".
+__device__ inline void wait_all_but_last_tile() { asm volatile("s_waitcnt vmcnt(8)" ::: "memory"); }
+__device__ inline void wait_all_loads() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 __device__ inline void wait_lds() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+__device__ inline void compiler_fence() { asm volatile("" ::: "memory"); }
 
 // max / sum of a value over the lane pair (l, l ^ 32) that shares a query
 __device__ inline float pair_max(float x) {
@@ -126,10 +142,13 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
                                                       const int32_t* __restrict__ cnt,
                                                       uint16_t* __restrict__ out,
                                                       float* __restrict__ lse, AttnArgs a) {
-  // LDS pointers stay in address space 3 (no generic-pointer casts)
-  __shared__ __attribute__((aligned(1024))) char smem[2 * 64 * 128];
-  lds_char* const ks = (lds_char*)smem;
-  lds_char* const vs = ks + 64 * 128;
+  // LDS pointers stay in address space 3 (no generic-pointer casts). K and V
+  // are separate objects, so the compiler can see that refilling one tile
+  // does not alias reads of the other.
+  __shared__ __attribute__((aligned(1024))) char k_tile[64 * 128];
+  __shared__ __attribute__((aligned(1024))) char v_tile[64 * 128];
+  lds_char* const ks = (lds_char*)k_tile;
+  lds_char* const vs = (lds_char*)v_tile;
 
   const Work w = work_item(a);
   if (!w.valid) return;
@@ -149,11 +168,6 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
   const __amdgpu_buffer_rsrc_t rv = make_rsrc(v + head_off, head_bytes);
   const __amdgpu_buffer_rsrc_t ro = make_rsrc(out + head_off, head_bytes);
 
-  const int dma_off = dma_lane_offset(lane);
-  int j = count > 0 ? (dense ? 0 : list[0]) : 0;
-  dma_tile(rk, j, ks, dma_off);
-  dma_tile(rv, j, vs, dma_off);
-
   // Q^T as the B operand: qB[tq][s] = Q[64i + 32tq + l32][16s + 8hf + (0..7)]
   bf16x8 qB[2][4];
 #pragma unroll
@@ -162,6 +176,13 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
     for (int s = 0; s < 4; ++s)
       qB[tq][s] = load_b128(
           rq, (uint32_t)(((w.i * kBlock + 32 * tq + l32) * kHeadDim + 16 * s + 8 * hf) * 2));
+
+  // load order from here on: K tile, V tile, next K tile, next V tile, ...
+  compiler_fence();
+  const DmaLaneOffsets dma_off = dma_lane_offset(lane);
+  int j = count > 0 ? (dense ? 0 : list[0]) : 0;
+  dma_tile(rk, j, ks, dma_off);
+  dma_tile(rv, j, vs, dma_off);
 
   f32x16 o[2][2];  // O^T tiles [head-dim half c][query half tq]
 #pragma unroll
@@ -182,11 +203,12 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
   // One step of the online softmax over kept tile `it`. Only the last step
   // can meet the partial last key block (lists are ascending), so only the
   // peeled last step carries the key mask.
-  auto step = [&](int it, auto masked) {
+  auto step = [&](int it, auto last) {
+    constexpr bool kLast = decltype(last)::value;
     const int jcur = j;
-    const bool more = it + 1 < count;
-    if (more) j = dense ? it + 1 : list[it + 1];
-    wait_dma();  // K and V of tile jcur are in LDS
+    constexpr bool more = !kLast;
+    if constexpr (more) j = dense ? it + 1 : list[it + 1];
+    wait_all_but_last_tile();  // the K tile of jcur is in LDS (its V tile may be in flight)
 
     // S^T[tk][tq] = K Q^T (keys 32tk.., queries 32tq..); K rows as A operand
     f32x16 s[2][2];
@@ -206,12 +228,12 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
       }
     }
     // the K operands are in registers: refill the K tile for the next step
-    if (more) {
+    if constexpr (more) {
       wait_lds();
       dma_tile(rk, j, ks, dma_off);
     }
 
-    if constexpr (decltype(masked)::value) {
+    if constexpr (kLast) {
       if (tail && jcur == nb - 1) {
         const int valid_keys = (int)(a.n - (int64_t)jcur * kBlock);
 #pragma unroll
@@ -270,6 +292,9 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
       l[tq] += rs;
     }
 
+    // the V tile of jcur is in LDS (the next K tile, if any, may be in flight)
+    if constexpr (more) wait_all_but_last_tile(); else wait_all_loads();
+
     // O^T[c][tq] += V^T[c][keys] P^T[keys][tq]
 #pragma unroll
     for (int tk = 0; tk < 2; ++tk)
@@ -290,7 +315,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
         }
       }
     // the V operands are consumed: refill the V tile for the next step
-    if (more) {
+    if constexpr (more) {
       wait_lds();
       dma_tile(rv, j, vs, dma_off);
     }
