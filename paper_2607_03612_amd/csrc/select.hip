@@ -66,17 +66,30 @@ __device__ inline QOperand load_q_operand(const double* qp_head, int i0, int nb,
 // i0 + lane/16 + 4e (the fp64 MFMA output order), key block 16c + lane%16. Always this instruction sequence, so a tile is
 // bit-identical whenever it is recomputed.
 // Columns past the last key block read a clamped (valid) address and are
-// never stored, so every load is unconditional and all 16 issue together.
-__device__ inline f64x4 score_tile(const QOperand& q, const double* kT, int nb, int c, int lane) {
+// never stored, so every load is unconditional.
+struct KColumn {
+  double b[16];
+};
+__device__ inline KColumn load_k_column(const double* kT, int nb, int c, int lane) {
   const int j = min(16 * c + (lane & 15), nb - 1);
   const double* col = kT + (int64_t)(lane >> 4) * nb + j;
-  double kb[16];
+  KColumn k;
 #pragma unroll
-  for (int s = 0; s < 16; ++s) kb[s] = col[(int64_t)(4 * s) * nb];
-  f64x4 acc = {0.0, 0.0, 0.0, 0.0};
+  for (int s = 0; s < 16; ++s) k.b[s] = col[(int64_t)(4 * s) * nb];
+  return k;
+}
+// 16x16 tile of raw scores (before the 1/8): element e of a lane is row
+// i0 + lane/16 + 4e (the fp64 MFMA output order), key block 16c + lane%16.
+// Two accumulation chains (even and odd dimension groups) summed at the end;
+// always this instruction sequence, so a recomputed tile is bit-identical.
+__device__ inline f64x4 score_tile(const QOperand& q, const KColumn& k) {
+  f64x4 a0 = {0.0, 0.0, 0.0, 0.0}, a1 = {0.0, 0.0, 0.0, 0.0};
 #pragma unroll
-  for (int s = 0; s < 16; ++s) acc = __builtin_amdgcn_mfma_f64_16x16x4f64(q.a[s], kb[s], acc, 0, 0, 0);
-  return acc;
+  for (int s = 0; s < 16; s += 2) {
+    a0 = __builtin_amdgcn_mfma_f64_16x16x4f64(q.a[s], k.b[s], a0, 0, 0, 0);
+    a1 = __builtin_amdgcn_mfma_f64_16x16x4f64(q.a[s + 1], k.b[s + 1], a1, 0, 0, 0);
+  }
+  return a0 + a1;
 }
 
 // Row of high keys of one query block, j = 64e + lane: in registers for the
@@ -98,6 +111,21 @@ struct RowKeys {
       for (int e = 0; e < MAXK; ++e) {
         const int j = 64 * e + lane;
         r[e] = j < nb ? row[j] : 0u;
+      }
+    }
+  }
+  // f(e, key) for every chunk e < chunks, from the registers (unrolled) or
+  // from LDS
+  template <typename F>
+  __device__ inline void each(F&& f, int nb) const {
+    if constexpr (MAXK > 0) {
+#pragma unroll
+      for (int e = 0; e < MAXK; ++e)
+        if (e < chunks) f(e, r[e]);
+    } else {
+      for (int e = 0; e < chunks; ++e) {
+        const int j = 64 * e + lane;
+        f(e, j < nb ? lds[j] : 0u);
       }
     }
   }
@@ -173,8 +201,11 @@ __global__ __launch_bounds__(THREADS) void select_topk_kernel(const double* __re
   const int chunks16 = (nb + 15) / 16;
   {
     const QOperand qa = load_q_operand(qp_head, i0, nb, lane);
+    KColumn next = load_k_column(kT, nb, min(wave, chunks16 - 1), lane);
     for (int c = wave; c < chunks16; c += kWaves) {
-      const f64x4 t = score_tile(qa, kT, nb, c, lane);
+      const KColumn cur = next;
+      next = load_k_column(kT, nb, min(c + kWaves, chunks16 - 1), lane);  // prefetch
+      const f64x4 t = score_tile(qa, cur);
       const int j = 16 * c + (lane & 15);
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
@@ -212,14 +243,12 @@ __global__ __launch_bounds__(THREADS) void select_topk_kernel(const double* __re
     for (int w = 0; w < kMaskWords; ++w) memb[w] = 0;
     if (k < nb) {
       uint32_t mn = 0xffffffffu, mx = 0u;
-      for (int e = 0; e < chunks; ++e) {
-        const int j = 64 * e + lane;
-        if (j < nb) {
-          const uint32_t x = lrow[j];
+      row.each([&](int, uint32_t x) {
+        if (x != 0u) {  // 0 marks a slot past the last block
           mn = min(mn, x);
           mx = max(mx, x);
         }
-      }
+      }, nb);
       mn = wave_min_u32(mn);
       mx = wave_max_u32(mx);
       int gt;
@@ -229,12 +258,11 @@ __global__ __launch_bounds__(THREADS) void select_topk_kernel(const double* __re
         take_ge = false;
         need = k - gt;
         int bucket = 0;
-        for (int e = 0; e < chunks; ++e) {
-          const int j = 64 * e + lane;
-          const bool m = j < nb && lrow[j] == T;
+        row.each([&](int e, uint32_t x) {
+          const bool m = x == T;
           if (m) memb[e >> 6] |= 1ull << (e & 63);
           bucket += __popcll(__ballot(m));
-        }
+        }, nb);
         if (bucket > need) {
           // stage 2: exact low halves of the bucket members from their
           // recomputed score tiles, written over the members' LDS slots
@@ -247,7 +275,7 @@ __global__ __launch_bounds__(THREADS) void select_topk_kernel(const double* __re
               const int b = __ffsll((unsigned long long)members) - 1;
               members &= members - 1;
               const int j = 64 * e + b;
-              const f64x4 t = score_tile(qa, kT, nb, j >> 4, lane);
+              const f64x4 t = score_tile(qa, load_k_column(kT, nb, j >> 4, lane));
               const double v = __shfl(t[r >> 2], (j & 15) + 16 * (r & 3));
               const uint32_t lo = (uint32_t)order_key(v * 0.125);
               if (lane == 0) lrow[j] = lo;
@@ -274,10 +302,11 @@ __global__ __launch_bounds__(THREADS) void select_topk_kernel(const double* __re
 
     int out_base = 0, eq_base = 0;
     const int take = stage2 ? need2 : need;
-    for (int e = 0; e < chunks; ++e) {
+    // slots past the last block hold key 0 < T and are never selected
+    row.each([&](int e, uint32_t key_hi) {
       const int j = 64 * e + lane;
       const bool member = (memb[e >> 6] >> (e & 63)) & 1;
-      const uint32_t x = member ? T : (j < nb ? lrow[j] : 0u);
+      const uint32_t x = member ? T : key_hi;
       bool sel, is_eq;
       if (take_ge) {
         sel = x >= T;
@@ -298,7 +327,7 @@ __global__ __launch_bounds__(THREADS) void select_topk_kernel(const double* __re
       if (sel && pos < a.cap) dst[pos] = j;
       out_base += __popcll(b_sel);
       eq_base += __popcll(b_eq);
-    }
+    }, nb);
     for (int p = out_base + lane; p < a.cap; p += 64) dst[p] = -1;
     if (lane == 0) cnt[(int64_t)h * nb + i0 + r] = out_base;
   }
