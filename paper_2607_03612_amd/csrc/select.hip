@@ -7,16 +7,22 @@
 // v_mfma_f64_16x16x4f64 with the pooled queries held in registers as the A
 // operand and the dimension-major pooled keys as coalesced B columns. Scores
 // become order-preserving 64-bit keys; LDS keeps only their high 32 bits.
-// One wave per query block then:
-//   1. loads its row of high keys into registers and finds, by bisection
-//      with wave-wide counts, the k-th largest high key T;
+// One wave per query block then, with its row of high keys in registers (lane
+// l holds blocks [l*C, l*C + C), C = ceil(nb / 64)):
+//   1. brackets the k-th largest high key between two pivots read off a
+//      stratified sample (one key per lane), checks the bracket with one
+//      counting pass and, once it holds at most 512 keys, packs those into
+//      LDS; bisection over the packed keys with wave-wide counts (per-lane
+//      VALU counts summed by a DPP scan) then finds the k-th largest high
+//      key T, or stops early at a threshold kept by exactly k keys;
 //   2. if more keys share T than are still needed, recomputes the score
 //      tiles of that bucket with the same instruction sequence (so the fp64
 //      values are bit-identical) and bisects their low 32 bits the same way
 //      (the low halves overwrite the bucket's LDS slots; a per-lane bitmask
 //      remembers the bucket, whose high half is T);
-//   3. compacts the kept indices in ascending order with ballots; keys equal
-//      in all 64 bits go to the lower block index.
+//   3. writes the kept indices in ascending order: a wave prefix sum of the
+//      per-lane kept counts gives each lane its output offset; keys equal in
+//      all 64 bits go to the lower block index.
 // The result equals a stable sort by (score desc, index asc), first k.
 //
 // Frame-local heads: the kept blocks of query block i are the contiguous
@@ -34,15 +40,25 @@ __device__ inline uint64_t order_key(double s) {
   return (b >> 63) ? ~b : (b | 0x8000000000000000ull);
 }
 
-__device__ inline uint32_t wave_min_u32(uint32_t v) {
-#pragma unroll
-  for (int m = 1; m < 64; m <<= 1) v = min(v, (uint32_t)__shfl_xor((int)v, m));
+// Lanes of one wave exchange values through LDS. The hardware runs a wave's
+// LDS instructions in order; this keeps the compiler from moving an LDS access
+// across the hand-over (it only sees each lane's own accesses).
+__device__ inline void wave_lds_handover() { asm volatile("" ::: "memory"); }
+
+// Inclusive prefix sum over the 64 lanes: shifts within rows of 16 lanes,
+// then the broadcasts of lane 15 into rows 1 and 3 and of lane 31 into rows 2
+// and 3 (DPP row_shr, row_bcast:15, row_bcast:31).
+__device__ inline uint32_t wave_scan_incl(uint32_t v) {
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x111, 0xf, 0xf, true);
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x112, 0xf, 0xf, true);
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x114, 0xf, 0xf, true);
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x118, 0xf, 0xf, true);
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x142, 0xa, 0xf, false);
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x143, 0xc, 0xf, false);
   return v;
 }
-__device__ inline uint32_t wave_max_u32(uint32_t v) {
-#pragma unroll
-  for (int m = 1; m < 64; m <<= 1) v = max(v, (uint32_t)__shfl_xor((int)v, m));
-  return v;
+__device__ inline uint32_t wave_total(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_readlane((int)wave_scan_incl(v), 63);
 }
 
 typedef double f64x4 __attribute__((ext_vector_type(4)));
@@ -92,63 +108,66 @@ __device__ inline f64x4 score_tile(const QOperand& q, const KColumn& k) {
   return a0 + a1;
 }
 
-// Row of high keys of one query block, j = 64e + lane: in registers for the
-// bisection counts when it has at most MAXK chunks of 64 (MAXK > 0), else
-// counted straight from LDS. Slots past the last block hold 0, below every
-// valid key.
+// Row of high keys of one query block; lane l owns blocks l*C + e, e < C.
+// Held in registers when C <= MAXK (MAXK > 0), else read from LDS on every
+// pass. Slots past the last block hold 0, below every valid key.
 template <int MAXK>
 struct RowKeys {
   uint32_t r[MAXK > 0 ? MAXK : 1];
   const uint32_t* lds;
-  int chunks, lane;
+  int C, base, nb;
 
-  __device__ inline void init(const uint32_t* row, int nb, int lane_) {
+  __device__ inline void init(const uint32_t* row, int nb_, int lane) {
     lds = row;
-    lane = lane_;
-    chunks = (nb + 63) / 64;
+    nb = nb_;
+    C = (nb + 63) / 64;
+    base = lane * C;
     if constexpr (MAXK > 0) {
 #pragma unroll
-      for (int e = 0; e < MAXK; ++e) {
-        const int j = 64 * e + lane;
-        r[e] = j < nb ? row[j] : 0u;
+      for (int e = 0; e < MAXK; ++e) r[e] = 0u;
+      // reads up to 64*C + 6 entries past the row start: the LDS holds
+      // kRowPad slack entries after the last row; slots e >= C belong to no
+      // block
+      each_slot([&](int e) {
+        const uint32_t x = row[base + e];
+        r[e] = e < C && base + e < nb ? x : 0u;
+      });
+    }
+  }
+  // g(e) for every slot e < C, in groups of 8 behind one uniform branch
+  template <typename G>
+  __device__ inline void each_slot(G&& g) const {
+#pragma unroll
+    for (int e0 = 0; e0 < MAXK; e0 += 8) {
+      if (e0 < C) {
+#pragma unroll
+        for (int e = e0; e < e0 + 8 && e < MAXK; ++e) g(e);
       }
     }
   }
-  // f(e, key) for every chunk e < chunks, from the registers (unrolled) or
-  // from LDS
+  // f(e, key) for every slot (padding slots included, with key 0)
   template <typename F>
-  __device__ inline void each(F&& f, int nb) const {
+  __device__ inline void each(F&& f) const {
     if constexpr (MAXK > 0) {
-#pragma unroll
-      for (int e = 0; e < MAXK; ++e)
-        if (e < chunks) f(e, r[e]);
+      each_slot([&](int e) { f(e, r[e]); });
     } else {
-      for (int e = 0; e < chunks; ++e) {
-        const int j = 64 * e + lane;
+      for (int e = 0; e < C; ++e) {
+        const int j = base + e;
         f(e, j < nb ? lds[j] : 0u);
       }
     }
   }
-  // number of keys >= t (t >= 1), wave-wide: one compare per chunk into a
-  // lane mask, popcounts summed on the scalar unit
-  __device__ inline int count_ge(uint32_t t, int nb) const {
-    int c = 0;
-    if constexpr (MAXK > 0) {
-#pragma unroll
-      for (int e = 0; e < MAXK; ++e) c += __popcll(__ballot(r[e] >= t));
-    } else {
-      for (int e = 0; e < chunks; ++e) {
-        const int j = 64 * e + lane;
-        c += __popcll(__ballot(j < nb && lds[j] >= t));
-      }
-    }
+  // this lane's keys >= t (t >= 1)
+  __device__ inline uint32_t lane_count_ge(uint32_t t) const {
+    uint32_t c = 0;
+    each([&](int, uint32_t x) { c += x >= t ? 1u : 0u; });
     return c;
   }
 };
 
-// k-th largest of the wave's 32-bit values (only lanes/elements passing
-// `valid` count). Returns T and sets *gt = number of values > T, or returns
-// with *exact set when {values >= T} has exactly k members.
+// k-th largest of the wave's 32-bit values by bisection over [lo, hi_incl]
+// (count_ge(lo) >= k). Returns T and sets *gt = number of values > T, or
+// returns with *exact set when {values >= T} has exactly k members.
 template <typename CountGe>
 __device__ inline uint32_t kth_largest(uint32_t lo, uint32_t hi_incl, int k, CountGe count_ge,
                                        int* gt, bool* exact) {
@@ -173,6 +192,15 @@ __device__ inline uint32_t kth_largest(uint32_t lo, uint32_t hi_incl, int k, Cou
   *gt = c_hi;
   return (uint32_t)lo64;
 }
+
+// LDS entries after the last row, so that every lane may read its C slots
+// rounded up to a multiple of 8 unconditionally.
+constexpr int kRowPad = 128;
+
+// Candidates packed per wave once the bracket holds at most this many keys
+// (8 per lane), and the pivots' distance from the target sample rank.
+constexpr int kPackedKeys = 512;
+constexpr int kPivotSlack = 4;
 
 template <int R, int THREADS, int MAXK>
 __global__ __launch_bounds__(THREADS) void select_topk_kernel(const double* __restrict__ qp,
@@ -221,115 +249,236 @@ __global__ __launch_bounds__(THREADS) void select_topk_kernel(const double* __re
   __syncthreads();
 
   // ---- selection: one wave per query block
-  const uint64_t lanemask_lt = (1ull << lane) - 1ull;
-  constexpr int kMaskWords = MAXK > 0 ? 1 : 4;  // chunks <= 48, or <= 256 (nb <= 16384)
+  constexpr int kMaskWords = MAXK > 0 ? 1 : 4;  // C <= 48, or <= 256 (nb <= 16384)
   for (int r = wave; r < rows; r += kWaves) {
     uint32_t* lrow = keys + r * nb;
     int32_t* dst = idx + ((int64_t)h * nb + i0 + r) * a.cap;
     RowKeys<MAXK> row;
     row.init(lrow, nb, lane);
-    const int chunks = row.chunks;
+    const int C = row.C;
 
-    // stage 1: T = k-th largest high key. Kept: hi > T, plus `need` of the
-    // hi == T bucket (all of it, or the best by stage 2)
+    // Kept: hi > T, plus `need` of the hi == T bucket (the best by stage 2),
+    // or every hi >= T when a threshold splits off exactly k keys.
     uint32_t T = 1;
-    bool take_ge = true;  // exact split: keep every hi >= T
+    bool take_ge = true;
     int need = 0;
-    bool stage2 = false;
     uint32_t T2 = 0;
     int need2 = 0;
-    uint64_t memb[kMaskWords];  // bit e of word e/64: slot (e, lane) is in the bucket
+    uint64_t memb[kMaskWords];  // bit e of word e/64: slot e of this lane is in the bucket
 #pragma unroll
     for (int w = 0; w < kMaskWords; ++w) memb[w] = 0;
     if (k < nb) {
-      uint32_t mn = 0xffffffffu, mx = 0u;
-      row.each([&](int, uint32_t x) {
-        if (x != 0u) {  // 0 marks a slot past the last block
-          mn = min(mn, x);
-          mx = max(mx, x);
-        }
-      }, nb);
-      mn = wave_min_u32(mn);
-      mx = wave_max_u32(mx);
-      int gt;
-      bool exact;
-      T = kth_largest(mn, mx, k, [&](uint32_t t) { return row.count_ge(t, nb); }, &gt, &exact);
-      if (!exact) {
-        take_ge = false;
-        need = k - gt;
-        int bucket = 0;
-        row.each([&](int e, uint32_t x) {
-          const bool m = x == T;
-          if (m) memb[e >> 6] |= 1ull << (e & 63);
-          bucket += __popcll(__ballot(m));
-        }, nb);
-        if (bucket > need) {
-          // stage 2: exact low halves of the bucket members from their
-          // recomputed score tiles, written over the members' LDS slots
-          stage2 = true;
-          const QOperand qa = load_q_operand(qp_head, i0, nb, lane);
-          uint32_t lmn = 0xffffffffu, lmx = 0u;
-          for (int e = 0; e < chunks; ++e) {
-            uint64_t members = __ballot((memb[e >> 6] >> (e & 63)) & 1);
-            while (members) {
-              const int b = __ffsll((unsigned long long)members) - 1;
-              members &= members - 1;
-              const int j = 64 * e + b;
-              const f64x4 t = score_tile(qa, load_k_column(kT, nb, j >> 4, lane));
-              const double v = __shfl(t[r >> 2], (j & 15) + 16 * (r & 3));
-              const uint32_t lo = (uint32_t)order_key(v * 0.125);
-              if (lane == 0) lrow[j] = lo;
-              lmn = min(lmn, lo);
-              lmx = max(lmx, lo);
+      // bracket: count(>= lo) > k > count(>= hi); thresholds are 33-bit so
+      // that hi = 2^32 (counted by nobody) fits
+      uint64_t lo = 1, hi = 1ull << 32;
+      int c_lo = nb, c_hi = 0;
+      bool exact = false;
+      if constexpr (MAXK > 8) {
+        if (C >= 8) {
+          // pivots from the sample of keys l*C (made distinct by the lane
+          // in the low 6 bits): ranks about kPivotSlack samples on either
+          // side of the expected rank k*64/nb of the k-th key
+          const uint32_t xs = (row.r[0] & 0xffffffc0u) | (uint32_t)lane;
+          wave_lds_handover();
+          lrow[lane] = xs;  // the row is in registers; its LDS is scratch now
+          wave_lds_handover();
+          int g = 0;
+#pragma unroll
+          for (int s2 = 0; s2 < 64; ++s2) g += lrow[s2] > xs ? 1 : 0;
+          const int64_t k64 = (int64_t)k * 64;
+          const int rank_hi = k64 >= (int64_t)kPivotSlack * nb
+                                  ? (int)((k64 - (int64_t)kPivotSlack * nb) / nb) : -1;
+          const int rank_lo = (int)((k64 + (int64_t)kPivotSlack * nb + nb - 1) / nb);
+          uint64_t p_lo = 1, p_hi = 1ull << 32;
+          if (rank_hi >= 0)
+            p_hi = (uint64_t)(uint32_t)__builtin_amdgcn_readlane(
+                       (int)xs, __builtin_ctzll(__ballot(g == rank_hi))) + 1;
+          if (rank_lo <= 63)
+            p_lo = max((uint32_t)__builtin_amdgcn_readlane(
+                           (int)xs, __builtin_ctzll(__ballot(g == rank_lo))) & 0xffffffc0u, 1u);
+          // one pass counts both pivots (count(>= p_lo) in the low half)
+          const bool hi_inf = p_hi >> 32;
+          const uint32_t t_lo = (uint32_t)p_lo, t_hi = (uint32_t)p_hi;
+          uint32_t pc = 0;
+          row.each([&](int, uint32_t x) {
+            pc += (x >= t_lo ? 1u : 0u) + (!hi_inf && x >= t_hi ? 0x10000u : 0u);
+          });
+          const uint32_t tot = wave_total(pc);
+          const int cl = (int)(tot & 0xffffu), ch = (int)(tot >> 16);
+          if (cl == k) {
+            exact = true;
+            T = t_lo;
+          } else if (!hi_inf && ch == k) {
+            exact = true;
+            T = t_hi;
+          } else {
+            if (ch > k) {
+              lo = p_hi;
+              c_lo = ch;
+            } else if (cl > k) {
+              lo = p_lo;
+              c_lo = cl;
+            }
+            if (cl < k) {
+              hi = p_lo;
+              c_hi = cl;
+            } else if (ch < k) {
+              hi = p_hi;
+              c_hi = ch;
             }
           }
-          auto count_lo = [&](uint32_t t) {
-            int c = 0;
-            for (int e = 0; e < chunks; ++e) {
-              const bool m = (memb[e >> 6] >> (e & 63)) & 1;
-              c += __popcll(__ballot(m && lrow[64 * e + lane] >= t));
-            }
-            return c;
-          };
-          int gt2;
-          bool exact2;
-          T2 = kth_largest(lmn, lmx, need, count_lo, &gt2, &exact2);
-          need2 = exact2 ? 0 : need - gt2;
-          if (exact2) T2 = T2 - 1;  // members with lo > T2 are exactly the ones needed
         }
+      }
+      bool packed = false;
+      int c_above = 0;  // keys at or above the packed bracket's top
+      uint32_t pk[kPackedKeys / 64];
+#pragma unroll
+      for (int q = 0; q < kPackedKeys / 64; ++q) pk[q] = 0u;
+      while (!exact && hi - lo > 1) {
+        if constexpr (MAXK > 8) {
+          // pack the bracket's keys into LDS slots [0, c_lo - c_hi); keys
+          // outside it go to a per-lane dummy slot at the row's end
+          if (!packed && C >= 10 && c_lo - c_hi <= kPackedKeys) {
+            const uint32_t lo32 = (uint32_t)lo, span = (uint32_t)(hi - lo - 1);
+            uint32_t n = 0;
+            row.each([&](int, uint32_t x) { n += x - lo32 <= span ? 1u : 0u; });
+            uint32_t pos = wave_scan_incl(n) - n;
+            const uint32_t dummy = (uint32_t)(nb - 64 + lane);
+            wave_lds_handover();
+            row.each([&](int, uint32_t x) {
+              const bool in = x - lo32 <= span;
+              lrow[in ? pos : dummy] = x;
+              pos += in ? 1u : 0u;
+            });
+            wave_lds_handover();
+            const int ncand = c_lo - c_hi;
+#pragma unroll
+            for (int q = 0; q < kPackedKeys / 64; ++q)
+              pk[q] = 64 * q + lane < ncand ? lrow[64 * q + lane] : 0u;
+            c_above = c_hi;
+            packed = true;
+          }
+        }
+        const uint64_t mid = lo + (hi - lo) / 2;
+        const uint32_t t = (uint32_t)mid;
+        int c;
+        if (packed) {
+          uint32_t n = 0;
+#pragma unroll
+          for (int q = 0; q < kPackedKeys / 64; ++q) n += pk[q] >= t ? 1u : 0u;
+          c = c_above + (int)wave_total(n);
+        } else {
+          c = (int)wave_total(row.lane_count_ge(t));
+        }
+        if (c == k) {
+          exact = true;
+          T = t;
+        } else if (c > k) {
+          lo = mid;
+          c_lo = c;
+        } else {
+          hi = mid;
+          c_hi = c;
+        }
+      }
+      if (!exact) {
+        // hi == lo + 1: the bucket of high key T holds c_lo - c_hi > need
+        // keys. Stage 2: exact low halves of its members from their
+        // recomputed score tiles, written over the members' LDS slots.
+        take_ge = false;
+        T = (uint32_t)lo;
+        need = k - c_hi;
+        row.each([&](int e, uint32_t x) {
+          if (x == T) memb[e >> 6] |= 1ull << (e & 63);
+        });
+        const QOperand qa = load_q_operand(qp_head, i0, nb, lane);
+        uint32_t lmn = 0xffffffffu, lmx = 0u;
+        wave_lds_handover();
+        for (int e = 0; e < C; ++e) {
+          uint64_t members = __ballot((memb[e >> 6] >> (e & 63)) & 1);
+          while (members) {
+            const int b = __ffsll((unsigned long long)members) - 1;
+            members &= members - 1;
+            const int j = b * C + e;
+            const f64x4 t = score_tile(qa, load_k_column(kT, nb, j >> 4, lane));
+            const double v = __shfl(t[r >> 2], (j & 15) + 16 * (r & 3));
+            const uint32_t lo_key = (uint32_t)order_key(v * 0.125);
+            if (lane == 0) lrow[j] = lo_key;
+            lmn = min(lmn, lo_key);
+            lmx = max(lmx, lo_key);
+          }
+        }
+        wave_lds_handover();
+        auto count_lo = [&](uint32_t t) {
+          uint32_t c = 0;
+          for (int e = 0; e < C; ++e) {
+            if ((memb[e >> 6] >> (e & 63)) & 1) c += lrow[min(row.base + e, nb - 1)] >= t ? 1u : 0u;
+          }
+          return (int)wave_total(c);
+        };
+        int gt2;
+        bool exact2;
+        T2 = kth_largest(lmn, lmx, need, count_lo, &gt2, &exact2);
+        need2 = exact2 ? 0 : need - gt2;
+        if (exact2) T2 = T2 - 1;  // members with lo > T2 are exactly the ones needed
       }
     }
 
-    int out_base = 0, eq_base = 0;
-    const int take = stage2 ? need2 : need;
-    // slots past the last block hold key 0 < T and are never selected
-    row.each([&](int e, uint32_t key_hi) {
-      const int j = 64 * e + lane;
+    // ascending output
+    if (MAXK > 0 && take_ge && k + 64 <= nb) {
+      // every key >= T, k of them: each lane writes its kept indices to LDS
+      // slots [0, k) from its prefix-sum offset (others to a dummy slot among
+      // the row's last 64), then the list goes out coalesced
+      const uint32_t n = row.lane_count_ge(T);
+      uint32_t pos = wave_scan_incl(n) - n;
+      const uint32_t dummy = (uint32_t)(nb - 64 + lane);
+      wave_lds_handover();
+      row.each([&](int e, uint32_t x) {
+        const bool kept = x >= T;
+        lrow[kept ? pos : dummy] = (uint32_t)(row.base + e);
+        pos += kept ? 1u : 0u;
+      });
+      wave_lds_handover();
+      for (int p = lane; p < a.cap; p += 64) dst[p] = p < k ? (int32_t)lrow[p] : -1;
+      if (lane == 0) cnt[(int64_t)h * nb + i0 + r] = k;
+      continue;
+    }
+    // general case: per-lane counts of keys kept outright (low half) and
+    // of tie-set keys (high half), prefix-summed over the wave
+    auto classify = [&](int e, uint32_t key_hi, bool* strict, bool* is_eq) {
       const bool member = (memb[e >> 6] >> (e & 63)) & 1;
-      const uint32_t x = member ? T : key_hi;
-      bool sel, is_eq;
       if (take_ge) {
-        sel = x >= T;
-        is_eq = false;
-      } else if (!stage2) {
-        is_eq = member;
-        sel = x > T;
+        *strict = key_hi >= T;
+        *is_eq = false;
       } else {
-        const uint32_t lo = member ? lrow[j] : 0u;
-        is_eq = member && lo == T2;
-        sel = x > T || (member && lo > T2);
+        const uint32_t lo_key = member ? lrow[min(row.base + e, nb - 1)] : 0u;
+        *strict = (!member && key_hi > T) || (member && lo_key > T2);
+        *is_eq = member && lo_key == T2;
       }
-      const uint64_t b_eq = __ballot(is_eq);
-      const int eq_before = eq_base + __popcll(b_eq & lanemask_lt);
-      sel = sel || (is_eq && eq_before < take);
-      const uint64_t b_sel = __ballot(sel);
-      const int pos = out_base + __popcll(b_sel & lanemask_lt);
-      if (sel && pos < a.cap) dst[pos] = j;
-      out_base += __popcll(b_sel);
-      eq_base += __popcll(b_eq);
-    }, nb);
-    for (int p = out_base + lane; p < a.cap; p += 64) dst[p] = -1;
-    if (lane == 0) cnt[(int64_t)h * nb + i0 + r] = out_base;
+    };
+    uint32_t packed_counts = 0;
+    row.each([&](int e, uint32_t key_hi) {
+      bool strict, is_eq;
+      classify(e, key_hi, &strict, &is_eq);
+      packed_counts += (strict ? 1u : 0u) + (is_eq ? 0x10000u : 0u);
+    });
+    const uint32_t incl = wave_scan_incl(packed_counts);
+    const uint32_t excl = incl - packed_counts;
+    const uint32_t total = (uint32_t)__builtin_amdgcn_readlane((int)incl, 63);
+    const int take = take_ge ? 0 : need2;
+    int eq_before = (int)(excl >> 16);
+    int pos = (int)(excl & 0xffffu) + min(eq_before, take);
+    const int out_total = (int)(total & 0xffffu) + min((int)(total >> 16), take);
+    row.each([&](int e, uint32_t key_hi) {
+      bool strict, is_eq;
+      classify(e, key_hi, &strict, &is_eq);
+      const bool sel = strict || (is_eq && eq_before < take);
+      if (sel && pos < a.cap) dst[pos] = row.base + e;
+      pos += sel ? 1 : 0;
+      eq_before += is_eq ? 1 : 0;
+    });
+    for (int p = out_total + lane; p < a.cap; p += 64) dst[p] = -1;
+    if (lane == 0) cnt[(int64_t)h * nb + i0 + r] = out_total;
   }
 }
 
@@ -386,7 +535,9 @@ hipError_t launch_topk_rows(const double* qp, const double* kpT, int32_t* idx, i
 
 }  // namespace
 
-size_t topk_lds_bytes(int rows, int nb) { return (size_t)rows * nb * sizeof(uint32_t); }
+size_t topk_lds_bytes(int rows, int nb) {
+  return ((size_t)rows * nb + kRowPad) * sizeof(uint32_t);
+}
 
 int topk_threads(int rows) { return rows >= 16 ? 512 : 256; }
 
