@@ -3,19 +3,22 @@
 // selected keys, and the softmax is renormalised over that set), with the
 // dense ("Full") case as the same loop over every key block.
 //
-// One wave owns one (head, 64-query block) and walks its kept-block list with
-// an online softmax:
+// One wave owns one (head, 64-query block) and walks its kept-block list in
+// half tiles of 32 keys with an online softmax:
 //   S^T = K Q^T      (keys x queries) on MFMA, so a lane owns one query
-//                    column and the row max / row sum stay inside the lane
-//                    pair (lane, lane ^ 32);
+//                    column and the row sum stays inside the lane pair
+//                    (lane, lane ^ 32);
 //   O^T += V^T P^T   (head dim x queries) on MFMA, P^T taken straight from
 //                    the S^T accumulators, V^T read from LDS with the gfx950
 //                    transposing LDS read so V is never transposed in memory.
-// Q sits in registers for the whole loop, K tiles are loaded straight into
-// the MFMA operand layout (prefetched one tile ahead), V goes through a
-// per-wave LDS tile. All global accesses use buffer instructions bounded by
-// the head's extent, so a partial last block reads zeros and a corrupt index
-// list cannot touch memory outside the head.
+// The half-tile steps are software-pipelined: step t issues S^T of half t+1
+// and the P V product of half t-1 on the matrix cores while the VALU runs
+// the softmax of half t, and the scheduler is told to interleave the two
+// streams. Q sits in registers for the whole loop; K and V half tiles are
+// staged in LDS by the direct buffer-to-LDS load two steps ahead. All global
+// accesses use buffer instructions bounded by the head's extent, so a
+// partial last block reads zeros and a corrupt index list cannot touch
+// memory outside the head.
 //
 // Launch order: workgroup b runs on XCD b % 8; each XCD takes a contiguous
 // slab of query blocks of every head (neighbouring query blocks share kept
@@ -76,7 +79,7 @@ typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(3))) char lds_char;
 typedef __attribute__((address_space(3))) const bf16x8 lds_bf16x8;
 
-// LDS tiles: 64 rows x 128 B; 16-byte chunk c of row r is stored at slot
+// LDS tiles: rows of 128 B; 16-byte chunk c of row r is stored at slot
 // c ^ f(r), f(r) = (bit2(r), bit1(r), bit0(r) ^ bit1(r) ^ bit3(r)). With it
 // the MFMA operand reads (16 rows at one chunk) and the transposing reads
 // (4 rows x 2 chunks per 16 lanes, 4 x 4 per 32) touch every bank once,
@@ -86,13 +89,12 @@ __device__ inline int swz_f(int r) {
 }
 __device__ inline int swz(int r, int c) { return r * 128 + ((c ^ swz_f(r)) << 4); }
 
-// One 64x64 bf16 tile (rows 64j.. of the head) into LDS with the direct
-// buffer-to-LDS load: instruction n fills LDS bytes [1024n, 1024n + 1024),
-// lane l its 16 bytes at 16l, i.e. row 8n + l/8, slot l%8, which must hold
-// chunk (l%8) ^ f(8n + l/8) = (l%8) ^ f(l/8) ^ (4 if n is odd). Rows past
-// the head read as zeros. The lane's byte offset inside its 8-row group
-// depends only on the parity of n; the tile and group offsets are
-// wave-uniform and go in the scalar offset.
+// Direct buffer-to-LDS loads of 8-row groups: instruction n fills LDS bytes
+// [1024n, 1024n + 1024), lane l its 16 bytes at 16l, i.e. row 8n + l/8,
+// slot l%8, which must hold chunk (l%8) ^ f(8n + l/8) = (l%8) ^ f(l/8) ^ (4
+// if n is odd). Rows past the head read as zeros. The lane's byte offset
+// inside its 8-row group depends only on the parity of n; the tile and
+// group offsets are wave-uniform and go in the scalar offset.
 struct DmaLaneOffsets {
   int even, odd;
 };
@@ -101,24 +103,6 @@ __device__ inline DmaLaneOffsets dma_lane_offset(int lane) {
   const int c = (lane & 7) ^ swz_f(r);
   return {(r * kHeadDim + c * 8) * 2, (r * kHeadDim + (c ^ 4) * 8) * 2};
 }
-__device__ inline void dma_tile(__amdgpu_buffer_rsrc_t r, int j, lds_char* tile,
-                                DmaLaneOffsets off) {
-  const int base = __builtin_amdgcn_readfirstlane(j * kBlock * kHeadDim * 2);  // j is wave-uniform
-#pragma unroll
-  for (int n = 0; n < 8; ++n)
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)(tile + 1024 * n), 16,
-                                             (n & 1) ? off.odd : off.even,
-                                             base + n * 8 * kHeadDim * 2, 0, 0);
-}
-
-// Waits on the direct-to-LDS loads. Vector memory loads complete in issue
-// order, and each tile is eight loads, so "all but the last eight" means "all
-// but the tile issued last".
-__device__ inline void wait_all_but_last_tile() { asm volatile("s_waitcnt vmcnt(8)" ::: "memory"); }
-__device__ inline void wait_all_loads() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
-__device__ inline void wait_lds() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
-__device__ inline void compiler_fence() { asm volatile("" ::: "memory"); }
-
 // max / sum of a value over the lane pair (l, l ^ 32) that shares a query
 __device__ inline float pair_max(float x) {
   const auto s = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
@@ -129,10 +113,25 @@ __device__ inline float pair_sum(float x) {
   return __uint_as_float(s[0]) + __uint_as_float(s[1]);
 }
 
-// The running max is only raised when a tile's max exceeds it by more than
-// this (log2 units): P stays <= 2^8 and O is rescaled rarely.
-constexpr float kRescaleSlack = 8.0f;
 constexpr bf16x2 kOnes = {(__bf16)1.0f, (__bf16)1.0f};
+
+// Waits expressed as s_waitcnt immediates (gfx9 encoding: vmcnt in bits 3:0
+// and 15:14, expcnt 6:4, lgkmcnt 11:8).
+constexpr int kWaitVm8 = 0x0F78;   // vmcnt(8)
+constexpr int kWaitVm0 = 0x0F70;   // vmcnt(0)
+constexpr int kWaitLgkm0 = 0xC07F; // lgkmcnt(0)
+
+// One 32-row half tile (rows 64j + 32h .. of the head) into an LDS half
+// buffer with the direct buffer-to-LDS load: four 1 KB instructions.
+__device__ inline void dma_half(__amdgpu_buffer_rsrc_t r, int j, int h, lds_char* buf,
+                                DmaLaneOffsets off) {
+  const int base = __builtin_amdgcn_readfirstlane((j * kBlock + 32 * h) * kHeadDim * 2);
+#pragma unroll
+  for (int n = 0; n < 4; ++n)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)(buf + 1024 * n), 16,
+                                             (n & 1) ? off.odd : off.even,
+                                             base + n * 8 * kHeadDim * 2, 0, 0);
+}
 
 template <bool kAllDense>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_bf16_kernel(const uint16_t* __restrict__ q,
@@ -142,13 +141,17 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
                                                       const int32_t* __restrict__ cnt,
                                                       uint16_t* __restrict__ out,
                                                       float* __restrict__ lse, AttnArgs a) {
-  // LDS pointers stay in address space 3 (no generic-pointer casts). K and V
-  // are separate objects, so the compiler can see that refilling one tile
-  // does not alias reads of the other.
-  __shared__ __attribute__((aligned(1024))) char k_tile[64 * 128];
-  __shared__ __attribute__((aligned(1024))) char v_tile[64 * 128];
-  lds_char* const ks = (lds_char*)k_tile;
-  lds_char* const vs = (lds_char*)v_tile;
+  // Four LDS half tiles of 32 rows: K half 0 / 1 and V half 0 / 1 of the
+  // tiles in flight. Separate objects, so the compiler sees which DMA writes
+  // can alias which reads.
+  __shared__ __attribute__((aligned(1024))) char k0_buf[32 * 128];
+  __shared__ __attribute__((aligned(1024))) char k1_buf[32 * 128];
+  __shared__ __attribute__((aligned(1024))) char v0_buf[32 * 128];
+  __shared__ __attribute__((aligned(1024))) char v1_buf[32 * 128];
+  lds_char* const kbuf0 = (lds_char*)k0_buf;
+  lds_char* const kbuf1 = (lds_char*)k1_buf;
+  lds_char* const vbuf0 = (lds_char*)v0_buf;
+  lds_char* const vbuf1 = (lds_char*)v1_buf;
 
   const Work w = work_item(a);
   if (!w.valid) return;
@@ -177,12 +180,13 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
       qB[tq][s] = load_b128(
           rq, (uint32_t)(((w.i * kBlock + 32 * tq + l32) * kHeadDim + 16 * s + 8 * hf) * 2));
 
-  // load order from here on: K tile, V tile, next K tile, next V tile, ...
-  compiler_fence();
   const DmaLaneOffsets dma_off = dma_lane_offset(lane);
-  int j = count > 0 ? (dense ? 0 : list[0]) : 0;
-  dma_tile(rk, j, ks, dma_off);
-  dma_tile(rv, j, vs, dma_off);
+  // tile of list position it, clamped to the last kept tile: loads past the
+  // end of the list refetch that tile into a buffer no later step reads
+  auto tile_at = [&](int it) -> int {
+    const int c = min(it, count - 1);
+    return dense ? c : list[c];
+  };
 
   f32x16 o[2][2];  // O^T tiles [head-dim half c][query half tq]
 #pragma unroll
@@ -194,134 +198,249 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
   float m[2] = {kNegInf, kNegInf};  // running max of the log2-scaled scores
   float l[2] = {0.f, 0.f};          // this lane's share of the running row sum
 
+  if (count <= 0) {  // an empty list: no keys, zero output, LSE -inf
+#pragma unroll
+    for (int tq = 0; tq < 2; ++tq) {
+      const int query = w.i * kBlock + 32 * tq + l32;
+#pragma unroll
+      for (int c = 0; c < 2; ++c)
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+          __builtin_amdgcn_raw_buffer_store_b64(i32x2{0, 0}, ro,
+              (int)((query * kHeadDim + 32 * c + 8 * g + 4 * hf) * 2), 0, 0);
+      if (lse && hf == 0 && query < a.n) lse[(int64_t)w.h * a.n + query] = kNegInf;
+    }
+    return;
+  }
+
   const bool tail = (a.n % kBlock) != 0;
+  const int valid_last = (int)(a.n - (int64_t)(nb - 1) * kBlock);  // keys in block nb-1
   const float sc = a.scale_log2;
   // transposing-read position of this lane inside a 4-row x 16-column group
   const int tr_row = 4 * hf + ((lane & 15) >> 2);
   const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
 
-  // One step of the online softmax over kept tile `it`. Only the last step
-  // can meet the partial last key block (lists are ascending), so only the
-  // peeled last step carries the key mask.
-  auto step = [&](int it, auto last) {
-    constexpr bool kLast = decltype(last)::value;
-    const int jcur = j;
-    constexpr bool more = !kLast;
-    if constexpr (more) j = dense ? it + 1 : list[it + 1];
-    wait_all_but_last_tile();  // the K tile of jcur is in LDS (its V tile may be in flight)
+  // ---- building blocks of one half-tile step
 
-    // S^T[tk][tq] = K Q^T (keys 32tk.., queries 32tq..); K rows as A operand
-    f32x16 s[2][2];
+  // S^T of a key half (32 keys x 64 queries) from an LDS K half buffer
+  auto read_k = [&](lds_char* kb, bf16x8 (&kA)[4]) {
 #pragma unroll
-    for (int tk = 0; tk < 2; ++tk) {
-      bf16x8 kA[4];
+    for (int st = 0; st < 4; ++st) kA[st] = *(lds_bf16x8*)(kb + swz(l32, 2 * st + hf));
+  };
+  auto read_v = [&](lds_char* vb, bf16x8 (&vA)[2][2]) {
 #pragma unroll
-      for (int st = 0; st < 4; ++st)
-        kA[st] = *(lds_bf16x8*)(ks + swz(32 * tk + l32, 2 * st + hf));
+    for (int u = 0; u < 2; ++u)
 #pragma unroll
-      for (int tq = 0; tq < 2; ++tq) {
-        f32x16 acc = {};
-#pragma unroll
-        for (int st = 0; st < 4; ++st)
-          acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kA[st], qB[tq][st], acc, 0, 0, 0);
-        s[tk][tq] = acc;
+      for (int c = 0; c < 2; ++c) {
+        const int krow = 16 * u + tr_row;
+        const int col = 32 * c + tr_col;
+        const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+            (lds_bf16x4*)(vb + swz(krow, col >> 3) + (col & 7) * 2));
+        const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+            (lds_bf16x4*)(vb + swz(krow + 8, col >> 3) + (col & 7) * 2));
+        vA[u][c] = bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
       }
-    }
-    // the K operands are in registers: refill the K tile for the next step
-    if constexpr (more) {
-      wait_lds();
-      dma_tile(rk, j, ks, dma_off);
-    }
-
-    if constexpr (kLast) {
-      if (tail && jcur == nb - 1) {
-        const int valid_keys = (int)(a.n - (int64_t)jcur * kBlock);
+  };
+  auto mfma_s = [&](const bf16x8 (&kA)[4], f32x16 (&s)[2]) {
+    f32x16 acc0 = {}, acc1 = {};
 #pragma unroll
-        for (int tk = 0; tk < 2; ++tk)
-#pragma unroll
-          for (int e = 0; e < 16; ++e) {
-            const int key = 32 * tk + 8 * (e >> 2) + 4 * hf + (e & 3);
-            if (key >= valid_keys) {
-              s[tk][0][e] = kNegInf;
-              s[tk][1][e] = kNegInf;
-            }
-          }
-      }
+    for (int st = 0; st < 4; ++st) {
+      acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kA[st], qB[0][st], acc0, 0, 0, 0);
+      acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kA[st], qB[1][st], acc1, 0, 0, 0);
     }
-
-    // online softmax per query column (lanes l and l ^ 32 share it). P is
-    // rounded to bf16 here, and the row sum adds the rounded values (one
-    // bf16 dot with (1, 1) per pair), so the normaliser matches the weights
-    // the P V product actually uses.
-    bf16x8 pB[2][2][2];  // [tk][u][tq]: keys 32tk + 16u.. as the B operand
+    s[0] = acc0;
+    s[1] = acc1;
+  };
+  auto mfma_pv = [&](const bf16x8 (&vA)[2][2], const bf16x8 (&p)[2][2]) {
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int c = 0; c < 2; ++c)
+#pragma unroll
+        for (int tq = 0; tq < 2; ++tq)
+          o[c][tq] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vA[u][c], p[u][tq], o[c][tq], 0, 0, 0);
+  };
+  // Online-softmax step over one key half. P = exp2(s*sc - m) is taken with
+  // the running max as it stands and rounded to bf16; the row sum adds the
+  // rounded values (one bf16 dot with (1, 1) per pair), so the normaliser
+  // matches the weights the P V product uses. Only when some lane's share of
+  // the row sum leaves [0, 2^12] (a new larger max, or the first half where
+  // the max is still -inf and the sum is inf or NaN) is the half's max taken:
+  // the running max moves to it, O and l are rescaled (after the P V of the
+  // previous half, which is already issued) and P is recomputed. Keys at or
+  // past `valid` (a partial last block) get P = 0.
+  auto probs = [&](const f32x16 (&s)[2], bf16x8 (&p)[2][2], float (&rs)[2]) {
 #pragma unroll
     for (int tq = 0; tq < 2; ++tq) {
-      float mx = fmaxf(fmaxf(s[0][tq][0], s[0][tq][1]), s[0][tq][2]);
+      const float mcur = m[tq];
+      float r = 0.f;
 #pragma unroll
-      for (int e = 3; e < 15; e += 2) mx = fmaxf(fmaxf(mx, s[0][tq][e]), s[0][tq][e + 1]);
-      mx = fmaxf(fmaxf(mx, s[0][tq][15]), s[1][tq][0]);
+      for (int u = 0; u < 2; ++u) {
+        bf16x2 pr[4];
 #pragma unroll
-      for (int e = 1; e < 15; e += 2) mx = fmaxf(fmaxf(mx, s[1][tq][e]), s[1][tq][e + 1]);
-      mx = fmaxf(mx, s[1][tq][15]);
-      const float tile_max = pair_max(mx) * sc;
-      const float mnew = tile_max > m[tq] + kRescaleSlack ? tile_max : m[tq];
-      if (__ballot(mnew != m[tq])) {  // wave-uniform: rescale only when some max moved
+        for (int e = 0; e < 4; ++e) {
+          const f32x2 pf = {fast_exp2(fmaf(s[tq][8 * u + 2 * e], sc, -mcur)),
+                            fast_exp2(fmaf(s[tq][8 * u + 2 * e + 1], sc, -mcur))};
+          pr[e] = __builtin_convertvector(pf, bf16x2);
+          r = __builtin_amdgcn_fdot2_f32_bf16(pr[e], kOnes, r, false);
+        }
+        p[u][tq] = bf16x8{pr[0][0], pr[0][1], pr[1][0], pr[1][1],
+                          pr[2][0], pr[2][1], pr[3][0], pr[3][1]};
+      }
+      rs[tq] = r;
+    }
+  };
+  auto mask_keys = [&](f32x16 (&s)[2], int valid) {
+    if (valid < 32) {
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int key = 8 * (e >> 2) + 4 * hf + (e & 3);
+        if (key >= valid) {
+          s[0][e] = kNegInf;
+          s[1][e] = kNegInf;
+        }
+      }
+    }
+  };
+  auto fixup = [&](f32x16 (&s)[2], bf16x8 (&p)[2][2], float (&rs)[2]) {
+    // 0x45800000 is 2^12; inf and NaN compare above it as unsigned bits
+    if (__ballot(__float_as_uint(rs[0]) > 0x45800000u || __float_as_uint(rs[1]) > 0x45800000u)) {
+#pragma unroll
+      for (int tq = 0; tq < 2; ++tq) {
+        float mx = fmaxf(fmaxf(s[tq][0], s[tq][1]), s[tq][2]);
+#pragma unroll
+        for (int e = 3; e < 15; e += 2) mx = fmaxf(fmaxf(mx, s[tq][e]), s[tq][e + 1]);
+        mx = fmaxf(mx, s[tq][15]);
+        const float mnew = fmaxf(pair_max(mx) * sc, m[tq]);
         const float alpha = fast_exp2(m[tq] - mnew);
         m[tq] = mnew;
         l[tq] *= alpha;
 #pragma unroll
         for (int c = 0; c < 2; ++c) o[c][tq] *= alpha;
       }
-      const float mcur = m[tq];
-      float rs = 0.f;
-#pragma unroll
-      for (int tk = 0; tk < 2; ++tk)
-#pragma unroll
-        for (int u = 0; u < 2; ++u) {
-          bf16x2 pr[4];
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const f32x2 pf = {fast_exp2(fmaf(s[tk][tq][8 * u + 2 * e], sc, -mcur)),
-                              fast_exp2(fmaf(s[tk][tq][8 * u + 2 * e + 1], sc, -mcur))};
-            pr[e] = __builtin_convertvector(pf, bf16x2);
-            rs = __builtin_amdgcn_fdot2_f32_bf16(pr[e], kOnes, rs, false);
-          }
-          pB[tk][u][tq] = bf16x8{pr[0][0], pr[0][1], pr[1][0], pr[1][1],
-                                 pr[2][0], pr[2][1], pr[3][0], pr[3][1]};
-        }
-      l[tq] += rs;
+      probs(s, p, rs);
     }
+    l[0] += rs[0];
+    l[1] += rs[1];
+  };
+  auto softmax = [&](f32x16 (&s)[2], int valid, bf16x8 (&p)[2][2]) {
+    mask_keys(s, valid);
+    float rs[2];
+    probs(s, p, rs);
+    fixup(s, p, rs);
+  };
 
-    // the V tile of jcur is in LDS (the next K tile, if any, may be in flight)
-    if constexpr (more) wait_all_but_last_tile(); else wait_all_loads();
+  // ---- pipeline
+  // Half-tile steps t = 2j + h (tile j of the list, key half h). Step t
+  // issues S^T of half t+1 and O += V^T P^T of half t-1 on the matrix cores
+  // while the VALU runs the softmax of half t, then refills the buffers it
+  // read: K half t+3 (same parity as t+1) and V half t+1 (parity of t-1).
+  // Every step issues eight DMA loads, so at the start of a step the loads
+  // of the step before last, which it reads, are done after vmcnt(8).
+  f32x16 s_cur[2];
+  bf16x8 p_prev[2][2];
+#pragma unroll
+  for (int u = 0; u < 2; ++u)
+#pragma unroll
+    for (int tq = 0; tq < 2; ++tq) p_prev[u][tq] = bf16x8{};  // P of half -1: nothing
 
-    // O^T[c][tq] += V^T[c][keys] P^T[keys][tq]
+  int j0 = tile_at(0), j1 = tile_at(1), j2 = tile_at(2);
+  {
+    // prologue: S^T of half 0, then the loads steps -2 and -1 would issue
+    dma_half(rk, j0, 0, kbuf0, dma_off);
+    __builtin_amdgcn_s_waitcnt(kWaitVm0);
+    bf16x8 kA[4];
+    read_k(kbuf0, kA);
+    mfma_s(kA, s_cur);
+    __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+    dma_half(rk, j0, 1, kbuf1, dma_off);   // K half 1 (tile 0)
+    dma_half(rv, j0, 1, vbuf1, dma_off);   // V of half -1: any tile (its P is 0)
+    dma_half(rk, j1, 0, kbuf0, dma_off);   // K half 2 (tile 1)
+    dma_half(rv, j0, 0, vbuf0, dma_off);   // V half 0 (tile 0)
+  }
+
+  // One step with the matrix-core and VALU work of the same step in one
+  // scheduling region. kNext: there is a half t+1; kMask: half t may be the
+  // partial last block.
+  auto step = [&](auto h_c, auto next_c, auto mask_c, int jcur, int jkn, int jvn) {
+    constexpr int h = decltype(h_c)::value;
+    constexpr bool kNext = decltype(next_c)::value;
+    constexpr bool kMask = decltype(mask_c)::value;
+    lds_char* const kb = h == 0 ? kbuf1 : kbuf0;  // K half t+1
+    lds_char* const vb = h == 0 ? vbuf1 : vbuf0;  // V half t-1
+    __builtin_amdgcn_s_waitcnt(kWaitVm8);
+    bf16x8 kA[4];
+    bf16x8 vA[2][2];
+    if constexpr (kNext) read_k(kb, kA);
+    read_v(vb, vA);
+    f32x16 s_next[2];
+    if constexpr (kNext) mfma_s(kA, s_next);
+    mfma_pv(vA, p_prev);
+    int valid = 32;
+    if constexpr (kMask) {
+      if (tail && jcur == nb - 1) valid = valid_last - 32 * h;
+    }
+    bf16x8 p_new[2][2];
+    mask_keys(s_cur, valid);
+    float rs[2];
+    probs(s_cur, p_new, rs);
+    // schedule of this region: the 12 LDS operand reads first (mask 0x100),
+    // ten softmax VALU ops (0x002) while they land, then each of the 16
+    // MFMAs (0x008) followed by five VALU ops, so the matrix cores and the
+    // VALU work on independent data side by side
+    __builtin_amdgcn_sched_group_barrier(0x100, 12, 0);
+    __builtin_amdgcn_sched_group_barrier(0x002, 10, 0);
 #pragma unroll
-    for (int tk = 0; tk < 2; ++tk)
+    for (int g = 0; g < 16; ++g) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);
+    }
+    fixup(s_cur, p_new, rs);
+    // refill the two buffers this step read
+    __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+    if constexpr (kNext) {
+      dma_half(rk, jkn, h ^ 1, kb, dma_off);
+      dma_half(rv, jvn, h ^ 1, vb, dma_off);
+    }
 #pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        const int krow = 32 * tk + 16 * u + tr_row;
+    for (int u = 0; u < 2; ++u)
 #pragma unroll
-        for (int c = 0; c < 2; ++c) {
-          const int col = 32 * c + tr_col;
-          const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
-              (lds_bf16x4*)(vs + swz(krow, col >> 3) + (col & 7) * 2));
-          const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
-              (lds_bf16x4*)(vs + swz(krow + 8, col >> 3) + (col & 7) * 2));
-          const bf16x8 vA = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-#pragma unroll
-          for (int tq = 0; tq < 2; ++tq)
-            o[c][tq] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vA, pB[tk][u][tq], o[c][tq], 0, 0, 0);
-        }
-      }
-    // the V operands are consumed: refill the V tile for the next step
-    if constexpr (more) {
-      wait_lds();
-      dma_tile(rv, j, vs, dma_off);
+      for (int tq = 0; tq < 2; ++tq) p_prev[u][tq] = p_new[u][tq];
+    if constexpr (kNext) {
+      s_cur[0] = s_next[0];
+      s_cur[1] = s_next[1];
     }
   };
-  for (int it = 0; it + 1 < count; ++it) step(it, std::false_type{});
-  if (count > 0) step(count - 1, std::true_type{});
+
+  using F = std::false_type;
+  using T = std::true_type;
+  using H0 = std::integral_constant<int, 0>;
+  using H1 = std::integral_constant<int, 1>;
+  for (int it = 0; it + 1 < count; ++it) {
+    // tiles it (j0), it+1 (j1), it+2 (j2)
+    const int j3 = tile_at(it + 3);
+    step(H0{}, T{}, F{}, j0, j1, j0);  // half 2it:   loads K(it+1,1), V(it,1)
+    step(H1{}, T{}, F{}, j0, j2, j1);  // half 2it+1: loads K(it+2,0), V(it+1,0)
+    j0 = j1;
+    j1 = j2;
+    j2 = j3;
+  }
+  // last tile: its halves may hold the partial last block
+  step(H0{}, T{}, T{}, j0, j1, j0);
+  {
+    // final step: no half t+1; O += V^T P^T of half t-1, softmax of half t,
+    // then the P V of half t itself
+    __builtin_amdgcn_s_waitcnt(kWaitVm0);
+    bf16x8 vA[2][2];
+    read_v(vbuf0, vA);
+    mfma_pv(vA, p_prev);
+    int valid = 32;
+    if (tail && j0 == nb - 1) valid = valid_last - 32;
+    bf16x8 p_new[2][2];
+    softmax(s_cur, valid, p_new);
+    read_v(vbuf1, vA);
+    mfma_pv(vA, p_new);
+  }
 
   // epilogue: normalise, round to bf16, store; log-sum-exp in natural log
 #pragma unroll
