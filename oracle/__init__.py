@@ -5,18 +5,29 @@ this package; the product path never does.
 """
 from .saf3r_oracle import *  # noqa: F401,F403
 from .saf3r_oracle import (  # noqa: F401
+    ANCHOR,
+    DENSE,
+    FRAME_LOCAL,
+    GLOBAL_PROBE,
+    STRIDE,
+    TOPK,
+    anchor_row,
     attend_block,
     attend_head,
+    attend_stride,
+    attend_tokens,
     block_range,
     block_scores,
     dense_attention,
     frame_local_row,
+    global_probe_row,
     kept_fraction,
     nmse,
     num_blocks,
     pool_blocks,
     run_layer,
     select_head,
+    stride_keys,
     to_f64,
     topk_row,
 )

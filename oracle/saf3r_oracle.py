@@ -18,17 +18,23 @@ fusion or reordering beyond what the definitions state:
 3. Selection per head class (Sec. 4.1 kernels; the class comes from the
    offline profile of Sec. 4.2): DENSE keeps every key block, FRAME_LOCAL (the
    static kernel) keeps the key blocks that share a frame with the query
-   block, TOPK (the query-probe kernel) keeps the ``k`` best-scoring key blocks
-   with ties broken towards the lower block index.
+   block, ANCHOR (the static kernel's anchor-frame example) keeps the key
+   blocks of one designated frame, TOPK (the query-probe kernel per query
+   block) keeps the ``k`` best-scoring key blocks with ties broken towards the
+   lower block index, GLOBAL_PROBE (the query-probe kernel as Sec. 4.3 states
+   it) ranks key blocks by the single mean query of the whole sequence and
+   gives every query block the same ``k`` blocks, STRIDE (the uniform sampling
+   kernel) keeps every ``s``-th key token.
 4. Attention restricted to the kept keys (Sec. 4.1, Query-Probe Top-K kernel):
-   softmax over the union of the kept key blocks' tokens, renormalised over
-   that set, times V.
+   softmax over the kept key tokens, renormalised over that set, times V.
 5. NMSE (Sec. 4.2, Eq. 1) between full and sparse outputs, as a quality
    report.
 
 Pins (checked by the CPU tests, not by this module): pooling+scores against
 the brute-force tile mean of S; Top-K against brute force over all k-subsets;
-frame-local lists against a hand-worked example and special cases; attention
+frame-local and anchor lists against hand-worked examples and token loops;
+the global probe against the column mean of the full S computed by brute
+force (the identity of Sec. 4.3); attention (block lists and strided keys)
 against a library softmax attention with an explicit token mask; NMSE
 against closed forms. Every function here is pinned.
 """
@@ -41,6 +47,9 @@ import numpy as np
 DENSE = 0
 FRAME_LOCAL = 1
 TOPK = 2
+ANCHOR = 3
+STRIDE = 4
+GLOBAL_PROBE = 5
 
 
 # --------------------------------------------------------------------------
@@ -123,13 +132,47 @@ def topk_row(scores_row: np.ndarray, k: int):
     return chosen.astype(np.int64), margin
 
 
+def anchor_row(anchor: int, n: int, tokens_per_frame: int, block: int) -> np.ndarray:
+    """Key blocks of the anchor frame (static kernel, Sec. 4.1: every query
+    attends to a designated anchor frame): the blocks that hold a token of
+    frame ``anchor``. The same for every query block."""
+    token_frame = np.arange(n) // tokens_per_frame
+    token_block = np.arange(n) // block
+    return np.unique(token_block[token_frame == anchor]).astype(np.int64)
+
+
+def global_probe_row(q_head: np.ndarray, k_head: np.ndarray, k: int, block: int):
+    """Query-probe Top-K as Sec. 4.3 states it: one probe per head, the mean
+    of all N queries; key block ``j`` scores ``qbar . kbar_j / sqrt(D)`` (the
+    mean of S over all queries and the keys of block ``j``) and the ``k`` best
+    blocks are kept (ties to the lower index) for every query block.
+
+    Returns (ascending indices, margin, probe scores)."""
+    d = q_head.shape[1]
+    qbar = q_head.sum(axis=0) / q_head.shape[0]
+    s = (pool_blocks(k_head, block) @ qbar) / math.sqrt(d)
+    sel, margin = topk_row(s, k)
+    return sel, margin, s
+
+
+def stride_keys(n: int, stride: int) -> np.ndarray:
+    """Key tokens kept by the uniform sampling kernel (Sec. 4.1): every
+    ``stride``-th token, starting at token 0."""
+    if stride < 1:
+        raise ValueError("stride must be >= 1")
+    return np.arange(0, n, stride, dtype=np.int64)
+
+
 def select_head(pattern: int, topk: int, q_head: np.ndarray, k_head: np.ndarray,
                 tokens_per_frame: int, block: int):
     """Kept key blocks of every query block of one head.
 
-    Returns (lists, margins, scores): ``lists[i]`` ascending int64, ``margins``
-    the Top-K margins (+inf for the other classes), ``scores`` the block score
-    matrix for Top-K heads (None otherwise)."""
+    ``topk`` is the class parameter: the kept block count (TOPK,
+    GLOBAL_PROBE), the anchor frame (ANCHOR) or the key stride (STRIDE).
+    Returns (lists, margins, scores): ``lists[i]`` ascending int64 (None for
+    STRIDE, which keeps tokens, not blocks), ``margins`` the Top-K margins
+    (+inf for the other classes), ``scores`` the block score matrix of a TOPK
+    head or the probe scores of a GLOBAL_PROBE head (None otherwise)."""
     n = q_head.shape[0]
     nb = num_blocks(n, block)
     margins = np.full(nb, math.inf)
@@ -146,6 +189,23 @@ def select_head(pattern: int, topk: int, q_head: np.ndarray, k_head: np.ndarray,
             sel, margins[i] = topk_row(s[i], topk)
             lists.append(sel)
         return lists, margins, s
+    if pattern == ANCHOR:
+        frames = -(-n // tokens_per_frame)
+        if not 0 <= topk < frames:
+            raise ValueError("anchor frame out of range")
+        row = anchor_row(topk, n, tokens_per_frame, block)
+        return [row for _ in range(nb)], margins, None
+    if pattern == GLOBAL_PROBE:
+        if not 1 <= topk <= nb:
+            raise ValueError("topk out of range")
+        sel, margin, s = global_probe_row(q_head, k_head, topk, block)
+        margins[:] = margin
+        return [sel for _ in range(nb)], margins, s
+    if pattern == STRIDE:
+        # token-level: no block list; attention uses stride_keys
+        if not 1 <= topk <= n:
+            raise ValueError("stride out of range")
+        return None, margins, None
     raise ValueError(f"unknown pattern {pattern}")
 
 
@@ -172,6 +232,24 @@ def attend_block(q_head: np.ndarray, k_head: np.ndarray, v_head: np.ndarray, i: 
     out = (e / denom) @ v_head[keys]
     lse = (zmax + np.log(denom))[:, 0]
     return out, lse
+
+
+def attend_tokens(q_head: np.ndarray, k_head: np.ndarray, v_head: np.ndarray, rows: range,
+                  keys: np.ndarray):
+    """Output rows and log-sum-exp of the query tokens ``rows`` over the key
+    tokens ``keys``: softmax of ``q . k / sqrt(D)`` over that set, times V."""
+    d = q_head.shape[1]
+    z = (q_head[rows.start:rows.stop] @ k_head[keys].T) / math.sqrt(d)
+    zmax = z.max(axis=1, keepdims=True)
+    e = np.exp(z - zmax)
+    denom = e.sum(axis=1, keepdims=True)
+    return (e / denom) @ v_head[keys], (zmax + np.log(denom))[:, 0]
+
+
+def attend_stride(q_head, k_head, v_head, stride: int):
+    """Every query over the uniformly sampled keys (Sec. 4.1)."""
+    n, d = q_head.shape
+    return attend_tokens(q_head, k_head, v_head, range(0, n), stride_keys(n, stride))
 
 
 def attend_head(q_head, k_head, v_head, lists, block: int):
@@ -210,7 +288,8 @@ def nmse(o_full: np.ndarray, o_sparse: np.ndarray) -> float:
 
 
 def kept_fraction(lists_per_head, nb: int) -> float:
-    """Fraction of (query block, key block) pairs kept over all heads."""
+    """Fraction of (query block, key block) pairs kept over all heads (heads
+    with block lists)."""
     kept = sum(len(x) for lists in lists_per_head for x in lists)
     return kept / (len(lists_per_head) * nb * nb)
 
@@ -231,10 +310,13 @@ def run_layer(q, k, v, table, tokens_per_frame: int, dtype: str, block: int = 64
         qh, kh = to_f64(q[h], dtype), to_f64(k[h], dtype)
         lists, margins, s = select_head(pattern, topk, qh, kh, tokens_per_frame, block)
         res["lists"][h], res["margins"][h], res["scores"][h] = lists, margins, s
-        if pattern == TOPK:
+        if pattern in (TOPK, GLOBAL_PROBE):
             res["q_pooled"][h] = pool_blocks(qh, block)
             res["k_pooled"][h] = pool_blocks(kh, block)
         if with_attention:
             vh = to_f64(v[h], dtype)
-            res["out"][h], res["lse"][h] = attend_head(qh, kh, vh, lists, block)
+            if pattern == STRIDE:
+                res["out"][h], res["lse"][h] = attend_stride(qh, kh, vh, topk)
+            else:
+                res["out"][h], res["lse"][h] = attend_head(qh, kh, vh, lists, block)
     return res

@@ -253,3 +253,85 @@ def test_run_layer_on_a_tiny_workload_is_consistent():
     assert [len(x) for x in res["lists"][2]] == [2] * 4
     # frames of 70 tokens: block 0 = frame 0 (tokens 0..63); frame 0 reaches block 1
     assert list(res["lists"][1][0]) == [0, 1]
+
+
+# ------------------------------------- anchor frame, global probe, stride
+
+
+def test_anchor_row_matches_token_bruteforce():
+    """Anchor-frame static pattern: the blocks holding a token of the anchor
+    frame, written with a plain token loop."""
+    for n, T, block in [(300, 100, 64), (257, 61, 16), (64, 64, 64), (130, 7, 8)]:
+        frames = -(-n // T)
+        for a in range(frames):
+            want = sorted({t // block for t in range(n) if t // T == a})
+            assert list(O.anchor_row(a, n, T, block)) == want
+
+
+def test_anchor_hand_worked_example():
+    # N=300, T=100, block 64: frame 1 is tokens 100..199 -> blocks 1 (64..127),
+    # 2 (128..191) and 3 (192..255); frame 2 (200..299) -> blocks 3 and 4
+    assert list(O.anchor_row(1, 300, 100, 64)) == [1, 2, 3]
+    assert list(O.anchor_row(2, 300, 100, 64)) == [3, 4]
+    assert list(O.anchor_row(0, 300, 100, 64)) == [0, 1]
+
+
+def _bruteforce_column_mean_block_scores(q, k, block):
+    """Sec. 4.3 by definition: S = QK^T/sqrt(D) in plain loops, its column mean
+    over all queries, then averaged over the tokens of each key block."""
+    n, d = len(q), len(q[0])
+    col = [sum(sum(q[t][e] * k[u][e] for e in range(d)) / math.sqrt(d) for t in range(n)) / n
+           for u in range(n)]
+    nb = (n + block - 1) // block
+    return [sum(col[u] for u in range(j * block, min(n, (j + 1) * block)))
+            / len(range(j * block, min(n, (j + 1) * block))) for j in range(nb)]
+
+
+@pytest.mark.parametrize("n,block,d,k", [(37, 8, 5, 2), (24, 4, 3, 6), (9, 9, 4, 1)])
+def test_global_probe_row_matches_column_mean_definition(n, block, d, k):
+    q, k_ = _rand((n, d), 21) + 0.5, _rand((n, d), 22) * 2.0
+    want_scores = np.array(_bruteforce_column_mean_block_scores(q.tolist(), k_.tolist(), block))
+    sel, margin, s = O.global_probe_row(q, k_, k, block)
+    np.testing.assert_allclose(s, want_scores, rtol=1e-12, atol=1e-12)
+    assert list(sel) == _bruteforce_topk(want_scores.tolist(), k)
+
+
+def test_global_probe_differs_from_per_block_probe():
+    """The global probe gives every query block one list; per-block probes
+    (TOPK) generally differ, so a class mix-up would show."""
+    n, d = 96, 8
+    g = np.random.default_rng(23)
+    q = g.standard_normal((n, d))
+    q[:48] += 3.0 * g.standard_normal(d)   # two groups of queries that prefer
+    q[48:] += 3.0 * g.standard_normal(d)   # different keys
+    k = g.standard_normal((n, d)) * 2.0
+    lists_g, _, _ = O.select_head(O.GLOBAL_PROBE, 2, q, k, 48, 16)
+    lists_t, _, _ = O.select_head(O.TOPK, 2, q, k, 48, 16)
+    assert all(list(x) == list(lists_g[0]) for x in lists_g)
+    assert any(list(x) != list(lists_g[0]) for x in lists_t)
+
+
+def test_stride_keys_and_fraction():
+    assert list(O.stride_keys(10, 3)) == [0, 3, 6, 9]
+    assert list(O.stride_keys(5, 1)) == [0, 1, 2, 3, 4]
+    assert list(O.stride_keys(7, 7)) == [0]
+    # kept fraction 1/s when s divides N (the #Keys column of the stride rows)
+    for n, s_ in [(4096, 64), (4096, 32), (1374, 2)]:
+        assert len(O.stride_keys(n, s_)) * s_ == n
+
+
+@pytest.mark.parametrize("n,stride", [(50, 3), (64, 64), (33, 1), (40, 7)])
+def test_stride_attention_matches_library_with_token_mask(n, stride):
+    d = 8
+    q, k, v = _rand((n, d), 31), _rand((n, d), 32) * 2.0, _rand((n, d), 33)
+    out, lse = O.attend_stride(q, k, v, stride)
+    mask = torch.zeros((n, n), dtype=torch.bool)
+    mask[:, ::stride] = True
+    tq, tk, tv = (torch.from_numpy(x)[None, None] for x in (q, k, v))
+    want = torch.nn.functional.scaled_dot_product_attention(tq, tk, tv, attn_mask=mask[None, None])[0, 0]
+    np.testing.assert_allclose(out, want.numpy(), rtol=1e-12, atol=1e-12)
+    z = q @ k[::stride].T / math.sqrt(d)
+    np.testing.assert_allclose(lse, scipy.special.logsumexp(z, axis=1), rtol=1e-12, atol=1e-12)
+    if stride == 1:
+        dense_out, _ = O.dense_attention(q, k, v)
+        np.testing.assert_allclose(out, dense_out, rtol=1e-12, atol=1e-12)
