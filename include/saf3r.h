@@ -44,28 +44,47 @@ typedef enum {
   SAF3R_ERR_UNSUPPORTED = -2,      /* head_dim or block other than 64, sizes beyond the limits */
   SAF3R_ERR_CAPACITY = -3,         /* cap smaller than saf3r_index_capacity() */
   SAF3R_ERR_HIP = -4,              /* the HIP runtime reported an error on launch */
-  SAF3R_ERR_BAD_TABLE = -5         /* unknown pattern class, or Top-K budget outside [1, nb] */
+  SAF3R_ERR_BAD_TABLE = -5         /* unknown pattern class, or a class parameter out of range */
 } saf3r_status;
 
 typedef enum { SAF3R_F32 = 0, SAF3R_BF16 = 1 } saf3r_dtype;
 
 /* Head pattern classes (Sec. 4.1 kernels; assignment from the offline
- * profile of Sec. 4.2):
- *   SAF3R_DENSE        full attention ("Full" in the ablations);
- *   SAF3R_FRAME_LOCAL  static kernel: a query block keeps every key block
- *                      that shares at least one frame with it (block
- *                      granularity, so a block straddling two frames keeps
- *                      the key blocks of both);
- *   SAF3R_TOPK         query-probe Top-K kernel (Sec. 4.3) at block level:
- *                      keep the topk_blocks key blocks j with the largest
- *                      score qbar_i . kbar_j / sqrt(64), ties to the lower j.
+ * profile of Sec. 4.2). `param` is the class parameter:
+ *   SAF3R_DENSE         full attention ("Full" in the ablations); param unused;
+ *   SAF3R_FRAME_LOCAL   static kernel: a query block keeps every key block
+ *                       that shares at least one frame with it (block
+ *                       granularity, so a block straddling two frames keeps
+ *                       the key blocks of both); param unused;
+ *   SAF3R_TOPK          query-probe Top-K kernel (Sec. 4.3) per query block:
+ *                       keep the param key blocks j with the largest score
+ *                       qbar_i . kbar_j / sqrt(64), ties to the lower j;
+ *                       param in [1, nb];
+ *   SAF3R_ANCHOR        static kernel, anchor-frame form (Sec. 4.1): every
+ *                       query block keeps the key blocks holding a token of
+ *                       frame param; param in [0, frames);
+ *   SAF3R_STRIDE        uniform sampling kernel (Sec. 4.1): every query
+ *                       attends to key tokens 0, s, 2s, ... with s = param;
+ *                       param in [1, N]; token granularity, no block list;
+ *   SAF3R_GLOBAL_PROBE  query-probe Top-K as Sec. 4.3 states it: one probe
+ *                       per head, the mean qbar of all N queries; keep the
+ *                       param key blocks with the largest qbar . kbar_j / 8,
+ *                       ties to the lower j, the same list for every query
+ *                       block; param in [1, nb].
  */
-typedef enum { SAF3R_DENSE = 0, SAF3R_FRAME_LOCAL = 1, SAF3R_TOPK = 2 } saf3r_pattern;
+typedef enum {
+  SAF3R_DENSE = 0,
+  SAF3R_FRAME_LOCAL = 1,
+  SAF3R_TOPK = 2,
+  SAF3R_ANCHOR = 3,
+  SAF3R_STRIDE = 4,
+  SAF3R_GLOBAL_PROBE = 5
+} saf3r_pattern;
 
 typedef struct {
-  int32_t pattern;     /* saf3r_pattern */
-  int32_t topk_blocks; /* SAF3R_TOPK: key blocks kept per query block, in [1, nb]; ignored otherwise */
-} saf3r_head_cfg;      /* host array [heads] */
+  int32_t pattern; /* saf3r_pattern */
+  int32_t param;   /* class parameter, see saf3r_pattern */
+} saf3r_head_cfg;  /* host array [heads] */
 
 typedef struct {
   int32_t heads;            /* 1 .. 256 */
@@ -80,12 +99,13 @@ typedef struct {
 int32_t saf3r_num_blocks(const saf3r_problem* problem);
 
 /* Smallest `cap` accepted by saf3r_select_blocks / saf3r_sparse_attention:
- * the longest kept-block list of any FRAME_LOCAL or TOPK head (at least 1),
- * or a negative saf3r_status. DENSE heads need no list. */
+ * the longest kept-block list of any FRAME_LOCAL, TOPK, ANCHOR or
+ * GLOBAL_PROBE head (at least 1), or a negative saf3r_status. DENSE and
+ * STRIDE heads need no list. */
 int32_t saf3r_index_capacity(const saf3r_problem* problem, const saf3r_head_cfg* table);
 
 /* Block pooling (Sec. 4.3: the probe of a set of queries is their mean).
- * For every TOPK head h, block b and dimension d:
+ * For every TOPK and GLOBAL_PROBE head h, block b and dimension d:
  *   q_pooled[h][b][d] = mean of Q[h][t][d] over the tokens t of block b
  *   k_pooled[h][d][b] = mean of K[h][t][d] likewise (dimension-major, so
  *                       that the scoring pass reads it coalesced)
@@ -93,7 +113,7 @@ int32_t saf3r_index_capacity(const saf3r_problem* problem, const saf3r_head_cfg*
  *   q, k      device, [heads, N, 64] of problem->dtype
  *   q_pooled  device, float64 [heads, nb, 64]
  *   k_pooled  device, float64 [heads, 64, nb]
- *   Entries of non-TOPK heads are left untouched.
+ *   Entries of the other heads are left untouched.
  * Returns SAF3R_OK, or an error with nothing enqueued. */
 saf3r_status saf3r_estimate_blocks(const saf3r_problem* problem, const saf3r_head_cfg* table,
                                    const void* q, const void* k,
@@ -105,26 +125,35 @@ saf3r_status saf3r_estimate_blocks(const saf3r_problem* problem, const saf3r_hea
  *   DENSE:        block_cnt[h][i] = nb; block_idx[h][i][:] left untouched
  *                 (attention treats the head as dense);
  *   FRAME_LOCAL:  the contiguous range of key blocks sharing a frame with i;
- *   TOPK:         the topk_blocks highest scores s[i][j] = qbar_i . kbar_j / 8
- *                 (computed in float64), ties to the lower j.
+ *   TOPK:         the param highest scores s[i][j] = qbar_i . kbar_j / 8
+ *                 (computed in float64), ties to the lower j;
+ *   ANCHOR:       the contiguous range of key blocks of frame param;
+ *   STRIDE:       block_cnt[h][i] = ceil(ceil(N / param) / 64), the number of
+ *                 64-key groups of the sampled keys; block_idx untouched;
+ *   GLOBAL_PROBE: the param highest probe scores qbar . kbar_j / 8 with qbar
+ *                 the mean of all N queries (float64), ties to the lower j,
+ *                 the same list in every row i.
  * Lists are written ascending, padded with -1 up to cap.
  *   q_pooled, k_pooled device float64, [heads, nb, 64] and [heads, 64, nb], as
- *                      written by saf3r_estimate_blocks (read for TOPK heads only)
+ *                      written by saf3r_estimate_blocks (read for TOPK and
+ *                      GLOBAL_PROBE heads only)
  *   block_idx          device int32 [heads, nb, cap]
  *   block_cnt          device int32 [heads, nb]
  *   cap                >= saf3r_index_capacity(problem, table)
  *   scores_or_null     NULL, or device float64 [heads, nb, nb]: the full score
- *                      matrix of every TOPK head (other heads untouched)
+ *                      matrix of every TOPK head; for a GLOBAL_PROBE head the
+ *                      probe scores in row 0 (other rows and heads untouched)
  * Returns SAF3R_OK, or an error with nothing enqueued. */
 saf3r_status saf3r_select_blocks(const saf3r_problem* problem, const saf3r_head_cfg* table,
                                  const double* q_pooled, const double* k_pooled,
                                  int32_t* block_idx, int32_t* block_cnt, int32_t cap,
                                  double* scores_or_null, void* stream);
 
-/* Attention restricted to the kept key blocks (Sec. 4.1: compute only the
- * scores between the queries and the selected keys, softmax renormalised
- * over them). For a query token t of block i of head h, with U the tokens of
- * the blocks listed for (h, i) (all blocks for a DENSE head):
+/* Attention restricted to the kept keys (Sec. 4.1: compute only the scores
+ * between the queries and the selected keys, softmax renormalised over
+ * them). For a query token t of block i of head h, with U the tokens of the
+ * blocks listed for (h, i) (all tokens for a DENSE head; tokens 0, s, 2s, ...
+ * for a STRIDE head with s = param):
  *   z_u    = q_t . k_u / 8,  u in U
  *   out[t] = sum_u softmax(z)_u v_u
  *   lse[t] = log(sum_u exp(z_u))            (natural log)
@@ -134,9 +163,9 @@ saf3r_status saf3r_select_blocks(const saf3r_problem* problem, const saf3r_head_
  * inputs: everything in fp32.
  *   q, k, v      device [heads, N, 64] of problem->dtype
  *   block_idx, block_cnt, cap   as written by saf3r_select_blocks; entries of
- *                DENSE heads are not read. A list that is not ascending,
- *                repeats a block or holds indices outside [0, nb) gives
- *                unspecified output values but no out-of-bounds access.
+ *                DENSE and STRIDE heads are not read. A list that is not
+ *                ascending, repeats a block or holds indices outside [0, nb)
+ *                gives unspecified output values but no out-of-bounds access.
  *   out          device [heads, N, 64] of problem->dtype
  *   lse_or_null  NULL, or device float32 [heads, N]
  * Returns SAF3R_OK, or an error with nothing enqueued. */

@@ -5,10 +5,12 @@ The compute path is the HIP library ``libsaf3r.so`` (C ABI in
 """
 from . import binding  # noqa: F401
 from .binding import (  # noqa: F401
+    ANCHOR,
     BF16,
     DENSE,
     F32,
     FRAME_LOCAL,
+    GLOBAL_PROBE,
     TOPK,
     Saf3rError,
     estimate_blocks,
@@ -18,4 +20,5 @@ from .binding import (  # noqa: F401
     run_layer,
     select_blocks,
     sparse_attention,
+    STRIDE,
 )

@@ -13,7 +13,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG, "libsaf3r.so")
 
 F32, BF16 = 0, 1
-DENSE, FRAME_LOCAL, TOPK = 0, 1, 2
+DENSE, FRAME_LOCAL, TOPK, ANCHOR, STRIDE, GLOBAL_PROBE = 0, 1, 2, 3, 4, 5
 HEAD_DIM = 64
 BLOCK = 64
 
@@ -33,7 +33,7 @@ class Problem(ctypes.Structure):
 
 
 class HeadCfg(ctypes.Structure):
-    _fields_ = [("pattern", ctypes.c_int32), ("topk_blocks", ctypes.c_int32)]
+    _fields_ = [("pattern", ctypes.c_int32), ("param", ctypes.c_int32)]
 
 
 class Saf3rError(RuntimeError):
@@ -87,9 +87,10 @@ def problem(heads: int, frames: int, tokens_per_frame: int, dtype: int) -> Probl
 
 
 def head_table(table) -> ctypes.Array:
+    """Per-head ``(pattern, param)`` pairs as the C array."""
     arr = (HeadCfg * len(table))()
-    for h, (pattern, topk) in enumerate(table):
-        arr[h] = HeadCfg(int(pattern), int(topk))
+    for h, (pattern, param) in enumerate(table):
+        arr[h] = HeadCfg(int(pattern), int(param))
     return arr
 
 
@@ -145,7 +146,7 @@ def index_capacity(table, frames, tokens_per_frame, dtype=BF16) -> int:
 def estimate_blocks(q, k, table, frames, tokens_per_frame, q_pooled=None, k_pooled=None,
                     stream=None):
     """Pooled Q ``[heads, nb, 64]`` and pooled K ``[heads, 64, nb]`` (float64;
-    Top-K heads only)."""
+    TOPK and GLOBAL_PROBE heads only)."""
     import torch
 
     _check_qkv(q, k)
@@ -192,7 +193,7 @@ def select_blocks(q_pooled, k_pooled, table, frames, tokens_per_frame, cap=None,
 
 def sparse_attention(q, k, v, table, frames, tokens_per_frame, block_idx=None, block_cnt=None,
                      out=None, want_lse=False, stream=None):
-    """Attention over the kept blocks: ``(out [H, N, 64], lse [H, N] float32 or None)``."""
+    """Attention over the kept keys: ``(out [H, N, 64], lse [H, N] float32 or None)``."""
     import torch
 
     _check_qkv(q, k, v)

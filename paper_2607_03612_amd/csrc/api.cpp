@@ -23,6 +23,7 @@ struct Shape {
   int heads;
   int64_t n;
   int nb;
+  int frames;
   int tokens_per_frame;
   int dtype;
 };
@@ -38,6 +39,7 @@ saf3r_status check_problem(const saf3r_problem* p, Shape* out) {
   out->heads = p->heads;
   out->n = n;
   out->nb = (int)((n + saf3r::kBlock - 1) / saf3r::kBlock);
+  out->frames = p->frames;
   out->tokens_per_frame = p->tokens_per_frame;
   out->dtype = p->dtype;
   return SAF3R_OK;
@@ -46,12 +48,20 @@ saf3r_status check_problem(const saf3r_problem* p, Shape* out) {
 saf3r_status check_table(const Shape& s, const saf3r_head_cfg* t) {
   if (!t) return SAF3R_ERR_INVALID_ARGUMENT;
   for (int h = 0; h < s.heads; ++h) {
+    const int32_t p = t[h].param;
     switch (t[h].pattern) {
       case SAF3R_DENSE:
       case SAF3R_FRAME_LOCAL:
         break;
       case SAF3R_TOPK:
-        if (t[h].topk_blocks < 1 || t[h].topk_blocks > s.nb) return SAF3R_ERR_BAD_TABLE;
+      case SAF3R_GLOBAL_PROBE:
+        if (p < 1 || p > s.nb) return SAF3R_ERR_BAD_TABLE;
+        break;
+      case SAF3R_ANCHOR:
+        if (p < 0 || p >= s.frames) return SAF3R_ERR_BAD_TABLE;
+        break;
+      case SAF3R_STRIDE:
+        if (p < 1 || (int64_t)p > s.n) return SAF3R_ERR_BAD_TABLE;
         break;
       default:
         return SAF3R_ERR_BAD_TABLE;
@@ -77,16 +87,27 @@ int max_frame_local_len(const Shape& s) {
   return best;
 }
 
+// Kept blocks of an ANCHOR head: the key blocks holding a token of frame a.
+int anchor_len(const Shape& s, int a) {
+  const int64_t lo = (int64_t)a * s.tokens_per_frame;
+  const int64_t hi = std::min<int64_t>(lo + s.tokens_per_frame, s.n) - 1;
+  return (int)(hi / saf3r::kBlock - lo / saf3r::kBlock + 1);
+}
+
 int capacity(const Shape& s, const saf3r_head_cfg* t) {
   int cap = 1;
   bool any_fl = false;
   for (int h = 0; h < s.heads; ++h) {
-    if (t[h].pattern == SAF3R_TOPK) cap = std::max(cap, t[h].topk_blocks);
-    if (t[h].pattern == SAF3R_FRAME_LOCAL) any_fl = true;
+    const int p = t[h].pattern;
+    if (p == SAF3R_TOPK || p == SAF3R_GLOBAL_PROBE) cap = std::max(cap, t[h].param);
+    if (p == SAF3R_ANCHOR) cap = std::max(cap, anchor_len(s, t[h].param));
+    if (p == SAF3R_FRAME_LOCAL) any_fl = true;
   }
   if (any_fl) cap = std::max(cap, max_frame_local_len(s));
   return cap;
 }
+
+bool pooled_class(int pattern) { return pattern == SAF3R_TOPK || pattern == SAF3R_GLOBAL_PROBE; }
 
 saf3r_status hip_status(hipError_t e) { return e == hipSuccess ? SAF3R_OK : SAF3R_ERR_HIP; }
 
@@ -122,7 +143,7 @@ saf3r_status saf3r_estimate_blocks(const saf3r_problem* problem, const saf3r_hea
   a.n = s.n;
   a.nb = s.nb;
   for (int h = 0; h < s.heads; ++h)
-    if (table[h].pattern == SAF3R_TOPK) a.head[a.n_heads++] = (int16_t)h;
+    if (pooled_class(table[h].pattern)) a.head[a.n_heads++] = (int16_t)h;
   return hip_status(saf3r::launch_pool(s.dtype, q, k, q_pooled, k_pooled, a,
                                        static_cast<hipStream_t>(stream)));
 }
@@ -148,13 +169,21 @@ saf3r_status saf3r_select_blocks(const saf3r_problem* problem, const saf3r_head_
   sa.nb = s.nb;
   sa.cap = cap;
   sa.tokens_per_frame = s.tokens_per_frame;
+  saf3r::GlobalArgs ga{};
+  ga.n = s.n;
+  ga.nb = s.nb;
+  ga.cap = cap;
   for (int h = 0; h < s.heads; ++h) {
     if (table[h].pattern == SAF3R_TOPK) {
       ta.head[ta.n_heads] = (int16_t)h;
-      ta.topk[ta.n_heads++] = table[h].topk_blocks;
+      ta.topk[ta.n_heads++] = table[h].param;
+    } else if (table[h].pattern == SAF3R_GLOBAL_PROBE) {
+      ga.head[ga.n_heads] = (int16_t)h;
+      ga.topk[ga.n_heads++] = table[h].param;
     } else {
       sa.head[sa.n_heads] = (int16_t)h;
-      sa.pattern[sa.n_heads++] = (int8_t)table[h].pattern;
+      sa.pattern[sa.n_heads] = (int8_t)table[h].pattern;
+      sa.param[sa.n_heads++] = table[h].param;
     }
   }
   // Query blocks scored per workgroup: the most (up to 16) whose score rows
@@ -168,6 +197,8 @@ saf3r_status saf3r_select_blocks(const saf3r_problem* problem, const saf3r_head_
 
   hipStream_t hs = static_cast<hipStream_t>(stream);
   hipError_t e = saf3r::launch_select_static(block_idx, block_cnt, sa, hs);
+  if (e != hipSuccess) return SAF3R_ERR_HIP;
+  e = saf3r::launch_select_global(q_pooled, k_pooled, block_idx, block_cnt, scores_or_null, ga, hs);
   if (e != hipSuccess) return SAF3R_ERR_HIP;
   e = saf3r::launch_select_topk(q_pooled, k_pooled, block_idx, block_cnt, scores_or_null, ta,
                                 lds, hs);
@@ -184,36 +215,66 @@ saf3r_status saf3r_sparse_attention(const saf3r_problem* problem, const saf3r_he
   st = check_table(s, table);
   if (st != SAF3R_OK) return st;
   if (!q || !k || !v || !out) return SAF3R_ERR_INVALID_ARGUMENT;
-  bool all_dense = true;
-  for (int h = 0; h < s.heads; ++h) all_dense = all_dense && table[h].pattern == SAF3R_DENSE;
-  if (!all_dense) {
+  bool needs_lists = false;
+  for (int h = 0; h < s.heads; ++h) {
+    const int p = table[h].pattern;
+    needs_lists = needs_lists || (p != SAF3R_DENSE && p != SAF3R_STRIDE);
+  }
+  if (needs_lists) {
     if (!block_idx || !block_cnt) return SAF3R_ERR_INVALID_ARGUMENT;
     if (cap < capacity(s, table)) return SAF3R_ERR_CAPACITY;
   }
 
+  // Two launches: heads with block lists or dense (one kernel, heads in
+  // decreasing per-row cost so the longest rows start first), then STRIDE
+  // heads (token-sampled keys).
   saf3r::AttnArgs a{};
   a.n = s.n;
   a.nb = s.nb;
   a.cap = cap;
-  a.heads = s.heads;
   a.slab = (s.nb + 7) / 8;
   a.scale_log2 = (float)(1.4426950408889634 / sqrt((double)saf3r::kHeadDim));
-  // heads in decreasing per-row cost (kept blocks per query block), so the
-  // longest rows start first
-  std::vector<int> cost(s.heads);
+  saf3r::AttnArgs sa = a;
+  std::vector<int> cost(s.heads, 0);
   const int fl_len = max_frame_local_len(s);
+  std::vector<int> listed, strided;
+  bool all_dense = true;
   for (int h = 0; h < s.heads; ++h) {
     const int p = table[h].pattern;
     a.dense[h] = p == SAF3R_DENSE ? 1 : 0;
-    cost[h] = p == SAF3R_DENSE ? s.nb : (p == SAF3R_TOPK ? table[h].topk_blocks : fl_len);
+    sa.stride[h] = p == SAF3R_STRIDE ? table[h].param : 1;
+    switch (p) {
+      case SAF3R_DENSE: cost[h] = s.nb; break;
+      case SAF3R_FRAME_LOCAL: cost[h] = fl_len; break;
+      case SAF3R_ANCHOR: cost[h] = anchor_len(s, table[h].param); break;
+      case SAF3R_STRIDE:
+        cost[h] = (int)((((s.n + table[h].param - 1) / table[h].param) + saf3r::kBlock - 1) / saf3r::kBlock);
+        break;
+      default: cost[h] = table[h].param; break;  // TOPK, GLOBAL_PROBE
+    }
+    if (p == SAF3R_STRIDE) {
+      strided.push_back(h);
+    } else {
+      listed.push_back(h);
+      all_dense = all_dense && p == SAF3R_DENSE;
+    }
   }
-  std::vector<int> order(s.heads);
-  std::iota(order.begin(), order.end(), 0);
-  std::stable_sort(order.begin(), order.end(), [&](int x, int y) { return cost[x] > cost[y]; });
-  for (int hh = 0; hh < s.heads; ++hh) a.order[hh] = (int16_t)order[hh];
+  auto by_cost = [&](int x, int y) { return cost[x] > cost[y]; };
+  std::stable_sort(listed.begin(), listed.end(), by_cost);
+  std::stable_sort(strided.begin(), strided.end(), by_cost);
+  a.heads = (int)listed.size();
+  a.mode = all_dense ? 1 : 0;
+  for (size_t i = 0; i < listed.size(); ++i) a.order[i] = (int16_t)listed[i];
+  sa.heads = (int)strided.size();
+  sa.mode = 2;
+  for (size_t i = 0; i < strided.size(); ++i) sa.order[i] = (int16_t)strided[i];
 
+  hipStream_t hs = static_cast<hipStream_t>(stream);
+  hipError_t e = saf3r::launch_attention(s.dtype, q, k, v, block_idx, block_cnt, out, lse_or_null,
+                                         a, hs);
+  if (e != hipSuccess) return SAF3R_ERR_HIP;
   return hip_status(saf3r::launch_attention(s.dtype, q, k, v, block_idx, block_cnt, out,
-                                            lse_or_null, a, static_cast<hipStream_t>(stream)));
+                                            lse_or_null, sa, hs));
 }
 
 const char* saf3r_status_string(int32_t status) {
@@ -223,7 +284,7 @@ const char* saf3r_status_string(int32_t status) {
     case SAF3R_ERR_UNSUPPORTED: return "unsupported (head_dim/block must be 64; size limits)";
     case SAF3R_ERR_CAPACITY: return "index capacity smaller than saf3r_index_capacity()";
     case SAF3R_ERR_HIP: return "HIP runtime error on launch";
-    case SAF3R_ERR_BAD_TABLE: return "bad pattern table (class or Top-K budget)";
+    case SAF3R_ERR_BAD_TABLE: return "bad pattern table (class or class parameter)";
     default: return "unknown status";
   }
 }

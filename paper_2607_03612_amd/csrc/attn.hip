@@ -133,7 +133,29 @@ __device__ inline void dma_half(__amdgpu_buffer_rsrc_t r, int j, int h, lds_char
                                              base + n * 8 * kHeadDim * 2, 0, 0);
 }
 
-template <bool kAllDense>
+// Key sets a launch walks: per-head lists or all blocks (kLists), every block
+// of every head (kAllDense), or the keys 0, s, 2s, ... of STRIDE heads taken
+// 64 at a time as virtual blocks (kStrided).
+enum AttnMode { kLists = 0, kAllDense = 1, kStrided = 2 };
+
+// One 32-row half of virtual key block j of a STRIDE head: key rows
+// (64j + 32h + r) * stride, r < 32, into an LDS half buffer (same slot layout
+// as dma_half). Rows at or past token n load as zeros (offset past the
+// buffer's extent).
+__device__ inline void dma_half_strided(__amdgpu_buffer_rsrc_t r, int j, int h, lds_char* buf,
+                                        int lane, int64_t stride, int64_t n, uint32_t head_bytes) {
+  const int rr = lane >> 3;
+  const int c = (lane & 7) ^ swz_f(rr);
+#pragma unroll
+  for (int g = 0; g < 4; ++g) {
+    const int64_t row = ((int64_t)j * kBlock + 32 * h + 8 * g + rr) * stride;
+    const uint32_t off = row < n ? (uint32_t)(row * kHeadDim * 2) + (uint32_t)(((g & 1) ? (c ^ 4) : c) * 16)
+                                 : head_bytes;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)(buf + 1024 * g), 16, (int)off, 0, 0, 0);
+  }
+}
+
+template <int kMode>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_bf16_kernel(const uint16_t* __restrict__ q,
                                                       const uint16_t* __restrict__ k,
                                                       const uint16_t* __restrict__ v,
@@ -159,9 +181,12 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
   const int l32 = lane & 31;
   const int hf = lane >> 5;
   const int nb = a.nb;
-  const bool dense = kAllDense || a.dense[w.h] != 0;
+  const bool dense = kMode != kLists || a.dense[w.h] != 0;
   const int32_t* list = idx + ((int64_t)w.h * nb + w.i) * a.cap;
-  int count = nb;
+  // STRIDE heads: nkeys sampled keys in count virtual blocks of 64
+  const int64_t stride = kMode == kStrided ? a.stride[w.h] : 1;
+  const int64_t nkeys = kMode == kStrided ? (a.n + stride - 1) / stride : a.n;
+  int count = kMode == kStrided ? (int)((nkeys + kBlock - 1) / kBlock) : nb;
   if (!dense) count = min(max(cnt[(int64_t)w.h * nb + w.i], 0), a.cap);
 
   const int64_t head_off = (int64_t)w.h * a.n * kHeadDim;
@@ -170,6 +195,12 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
   const __amdgpu_buffer_rsrc_t rk = make_rsrc(k + head_off, head_bytes);
   const __amdgpu_buffer_rsrc_t rv = make_rsrc(v + head_off, head_bytes);
   const __amdgpu_buffer_rsrc_t ro = make_rsrc(out + head_off, head_bytes);
+  auto load_half = [&](__amdgpu_buffer_rsrc_t r, int j, int h, lds_char* buf, DmaLaneOffsets off) {
+    if constexpr (kMode == kStrided)
+      dma_half_strided(r, j, h, buf, threadIdx.x, stride, a.n, head_bytes);
+    else
+      dma_half(r, j, h, buf, off);
+  };
 
   // Q^T as the B operand: qB[tq][s] = Q[64i + 32tq + l32][16s + 8hf + (0..7)]
   bf16x8 qB[2][4];
@@ -213,8 +244,10 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
     return;
   }
 
-  const bool tail = (a.n % kBlock) != 0;
-  const int valid_last = (int)(a.n - (int64_t)(nb - 1) * kBlock);  // keys in block nb-1
+  // the last (virtual) key block may hold fewer than 64 keys
+  const int last_block = kMode == kStrided ? count - 1 : nb - 1;
+  const bool tail = (nkeys % kBlock) != 0;
+  const int valid_last = (int)(nkeys - (int64_t)last_block * kBlock);
   const float sc = a.scale_log2;
   // transposing-read position of this lane inside a 4-row x 16-column group
   const int tr_row = 4 * hf + ((lane & 15) >> 2);
@@ -347,16 +380,16 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
   int j0 = tile_at(0), j1 = tile_at(1), j2 = tile_at(2);
   {
     // prologue: S^T of half 0, then the loads steps -2 and -1 would issue
-    dma_half(rk, j0, 0, kbuf0, dma_off);
+    load_half(rk, j0, 0, kbuf0, dma_off);
     __builtin_amdgcn_s_waitcnt(kWaitVm0);
     bf16x8 kA[4];
     read_k(kbuf0, kA);
     mfma_s(kA, s_cur);
     __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
-    dma_half(rk, j0, 1, kbuf1, dma_off);   // K half 1 (tile 0)
-    dma_half(rv, j0, 1, vbuf1, dma_off);   // V of half -1: any tile (its P is 0)
-    dma_half(rk, j1, 0, kbuf0, dma_off);   // K half 2 (tile 1)
-    dma_half(rv, j0, 0, vbuf0, dma_off);   // V half 0 (tile 0)
+    load_half(rk, j0, 1, kbuf1, dma_off);   // K half 1 (tile 0)
+    load_half(rv, j0, 1, vbuf1, dma_off);   // V of half -1: any tile (its P is 0)
+    load_half(rk, j1, 0, kbuf0, dma_off);   // K half 2 (tile 1)
+    load_half(rv, j0, 0, vbuf0, dma_off);   // V half 0 (tile 0)
   }
 
   // One step with the matrix-core and VALU work of the same step in one
@@ -378,7 +411,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
     mfma_pv(vA, p_prev);
     int valid = 32;
     if constexpr (kMask) {
-      if (tail && jcur == nb - 1) valid = valid_last - 32 * h;
+      if (tail && jcur == last_block) valid = valid_last - 32 * h;
     }
     bf16x8 p_new[2][2];
     mask_keys(s_cur, valid);
@@ -399,8 +432,8 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
     // refill the two buffers this step read
     __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
     if constexpr (kNext) {
-      dma_half(rk, jkn, h ^ 1, kb, dma_off);
-      dma_half(rv, jvn, h ^ 1, vb, dma_off);
+      load_half(rk, jkn, h ^ 1, kb, dma_off);
+      load_half(rv, jvn, h ^ 1, vb, dma_off);
     }
 #pragma unroll
     for (int u = 0; u < 2; ++u)
@@ -435,7 +468,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
     read_v(vbuf0, vA);
     mfma_pv(vA, p_prev);
     int valid = 32;
-    if (tail && j0 == nb - 1) valid = valid_last - 32;
+    if (tail && j0 == last_block) valid = valid_last - 32;
     bf16x8 p_new[2][2];
     softmax(s_cur, valid, p_new);
     read_v(vbuf1, vA);
@@ -468,6 +501,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
 
 // Same structure with v_mfma_f32_32x32x2_f32 and fp32 softmax operands; K and
 // V tiles both go through LDS (one wave, no barrier).
+template <int kMode>
 __global__ __launch_bounds__(64) void attn_f32_kernel(const float* __restrict__ q,
                                                      const float* __restrict__ k,
                                                      const float* __restrict__ v,
@@ -484,10 +518,13 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(const float* __restrict__ 
   const int l32 = lane & 31;
   const int hf = lane >> 5;
   const int nb = a.nb;
-  const bool dense = a.dense[w.h] != 0;
+  const bool dense = kMode != kLists || a.dense[w.h] != 0;
   const int32_t* list = idx + ((int64_t)w.h * nb + w.i) * a.cap;
-  int count = nb;
+  const int64_t stride = kMode == kStrided ? a.stride[w.h] : 1;
+  const int64_t nkeys = kMode == kStrided ? (a.n + stride - 1) / stride : a.n;
+  int count = kMode == kStrided ? (int)((nkeys + kBlock - 1) / kBlock) : nb;
   if (!dense) count = min(max(cnt[(int64_t)w.h * nb + w.i], 0), a.cap);
+  const int last_block = kMode == kStrided ? count - 1 : nb - 1;
 
   const int64_t head_off = (int64_t)w.h * a.n * kHeadDim;
   const uint32_t head_bytes = (uint32_t)(a.n * kHeadDim * 4);
@@ -523,16 +560,21 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(const float* __restrict__ 
       for (int e = 0; e < 16; ++e) o[c][tq][e] = 0.f;
   float m[2] = {kNegInf, kNegInf};
   float l[2] = {0.f, 0.f};
-  const bool tail = (a.n % kBlock) != 0;
+  const bool tail = (nkeys % kBlock) != 0;
   const float sc = a.scale_log2;
 
   for (int it = 0; it < count; ++it) {
     const int j = dense ? it : list[it];
-    // stage K and V tiles: rows 4n + lane/16, float4 chunk lane%16
+    // stage K and V tiles: rows 4n + lane/16, float4 chunk lane%16 (a STRIDE
+    // head's row r of virtual block j is token (64j + r) * stride; tokens at
+    // or past n read as zeros through an offset past the buffer's extent)
 #pragma unroll
     for (int n4 = 0; n4 < 16; ++n4) {
       const int row = 4 * n4 + (lane >> 4);
-      const int off = ((j * kBlock + row) * kHeadDim + (lane & 15) * 4) * 4;
+      const int64_t tok = ((int64_t)j * kBlock + row) * stride;
+      const int off = kMode == kStrided && tok >= a.n
+                          ? (int)head_bytes
+                          : (int)((tok * kHeadDim + (lane & 15) * 4) * 4);
       const f32x4 kx = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rk, off, 0, 0));
       const f32x4 vx = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rv, off, 0, 0));
 #pragma unroll
@@ -555,8 +597,8 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(const float* __restrict__ 
         s[tk][tq] = acc;
       }
 
-    if (tail && j == nb - 1) {
-      const int valid_keys = (int)(a.n - (int64_t)j * kBlock);
+    if (tail && j == last_block) {
+      const int valid_keys = (int)(nkeys - (int64_t)j * kBlock);
 #pragma unroll
       for (int tk = 0; tk < 2; ++tk)
 #pragma unroll
@@ -637,18 +679,18 @@ hipError_t launch_attention(int dtype, const void* q, const void* k, const void*
                             const AttnArgs& a, hipStream_t s) {
   const int64_t groups = 8LL * a.heads * a.slab;
   if (groups == 0) return hipSuccess;
-  bool all_dense = true;
-  for (int h = 0; h < a.heads; ++h) all_dense = all_dense && a.dense[h];
+  const dim3 grid((unsigned)groups);
   if (dtype == 1) {
-    auto kern = all_dense ? attn_bf16_kernel<true> : attn_bf16_kernel<false>;
-    hipLaunchKernelGGL(kern, dim3((unsigned)groups), dim3(64), 0, s,
-                       static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
-                       static_cast<const uint16_t*>(v), idx, cnt, static_cast<uint16_t*>(out),
-                       lse, a);
+    auto kern = a.mode == kStrided ? attn_bf16_kernel<kStrided>
+                : a.mode == kAllDense ? attn_bf16_kernel<kAllDense> : attn_bf16_kernel<kLists>;
+    hipLaunchKernelGGL(kern, grid, dim3(64), 0, s, static_cast<const uint16_t*>(q),
+                       static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v), idx, cnt,
+                       static_cast<uint16_t*>(out), lse, a);
   } else {
-    hipLaunchKernelGGL(attn_f32_kernel, dim3((unsigned)groups), dim3(64), 0, s,
-                       static_cast<const float*>(q), static_cast<const float*>(k),
-                       static_cast<const float*>(v), idx, cnt, static_cast<float*>(out), lse, a);
+    auto kern = a.mode == kStrided ? attn_f32_kernel<kStrided> : attn_f32_kernel<kLists>;
+    hipLaunchKernelGGL(kern, grid, dim3(64), 0, s, static_cast<const float*>(q),
+                       static_cast<const float*>(k), static_cast<const float*>(v), idx, cnt,
+                       static_cast<float*>(out), lse, a);
   }
   return hipGetLastError();
 }

@@ -11,7 +11,14 @@ constexpr int kBlock = 64;
 constexpr int kMaxHeads = 256;
 constexpr int kMaxBlocks = 16384;  // select keeps one score row per query block in LDS
 
-enum Pattern : int32_t { kDense = 0, kFrameLocal = 1, kTopK = 2 };
+enum Pattern : int32_t {
+  kDense = 0,
+  kFrameLocal = 1,
+  kTopK = 2,
+  kAnchor = 3,
+  kStride = 4,
+  kGlobalProbe = 5
+};
 
 // ---------------------------------------------------------------- launches
 
@@ -40,17 +47,30 @@ struct StaticArgs {
   int32_t n_heads;
   int16_t head[kMaxHeads];
   int8_t pattern[kMaxHeads];
+  int32_t param[kMaxHeads];  // ANCHOR: anchor frame; STRIDE: key stride
+};
+
+// Paper-literal query probe: one probe per head over all N queries.
+struct GlobalArgs {
+  int64_t n;
+  int32_t nb;
+  int32_t cap;
+  int32_t n_heads;
+  int16_t head[kMaxHeads];
+  int32_t topk[kMaxHeads];
 };
 
 struct AttnArgs {
   int64_t n;
   int32_t nb;
   int32_t cap;
-  int32_t heads;
+  int32_t heads;          // heads in this launch (entries of order[])
   int32_t slab;           // query blocks of one head handled by one XCD: ceil(nb / 8)
+  int32_t mode;           // 0: lists or dense per head; 1: every head dense; 2: STRIDE heads
   float scale_log2;       // log2(e) / sqrt(64)
-  int16_t order[kMaxHeads];   // heads, most expensive first
-  int8_t dense[kMaxHeads];    // per head: 1 = iterate all key blocks
+  int16_t order[kMaxHeads];   // heads of this launch, most expensive first
+  int8_t dense[kMaxHeads];    // by head index: 1 = iterate all key blocks
+  int32_t stride[kMaxHeads];  // by head index: key stride of a STRIDE head
 };
 
 hipError_t launch_pool(int dtype, const void* q, const void* k, double* qp, double* kp,
@@ -58,6 +78,8 @@ hipError_t launch_pool(int dtype, const void* q, const void* k, double* qp, doub
 hipError_t launch_select_topk(const double* qp, const double* kpT, int32_t* idx, int32_t* cnt,
                               double* scores, const TopKArgs& a, size_t lds_bytes, hipStream_t s);
 hipError_t launch_select_static(int32_t* idx, int32_t* cnt, const StaticArgs& a, hipStream_t s);
+hipError_t launch_select_global(const double* qp, const double* kpT, int32_t* idx, int32_t* cnt,
+                                double* scores, const GlobalArgs& a, hipStream_t s);
 hipError_t launch_attention(int dtype, const void* q, const void* k, const void* v,
                             const int32_t* idx, const int32_t* cnt, void* out, float* lse,
                             const AttnArgs& a, hipStream_t s);

@@ -27,6 +27,15 @@
 //
 // Frame-local heads: the kept blocks of query block i are the contiguous
 // range of key blocks whose tokens overlap the frames touched by block i.
+// Anchor heads: the contiguous range of key blocks of the anchor frame.
+//
+// Global-probe heads (the query probe of Sec. 4.3 as stated: one probe, the
+// mean of all N queries, per head): one workgroup per head forms the probe
+// from the pooled queries (sum of n_b * qbar_b over the blocks, over N),
+// scores every key block in float64, finds the k-th largest order key exactly
+// by an 8-bit-digit radix select over the 64-bit keys, writes the kept
+// blocks ascending (keys equal to the k-th go to the lowest indices), and a
+// second launch copies that list to every query block.
 #include "saf3r_internal.h"
 
 namespace saf3r {
@@ -482,7 +491,8 @@ __global__ __launch_bounds__(THREADS) void select_topk_kernel(const double* __re
   }
 }
 
-// One wave per (head, query block) of the non-Top-K heads.
+// One wave per (head, query block) of the static-pattern heads (DENSE,
+// FRAME_LOCAL, ANCHOR, STRIDE).
 __global__ __launch_bounds__(kStaticThreads) void select_static_kernel(int32_t* __restrict__ idx,
                                                                       int32_t* __restrict__ cnt,
                                                                       StaticArgs a) {
@@ -494,20 +504,160 @@ __global__ __launch_bounds__(kStaticThreads) void select_static_kernel(int32_t* 
   const int i = (int)(wave - (int64_t)slot * a.nb);
   const int h = a.head[slot];
   const int64_t row = (int64_t)h * a.nb + i;
-  if (a.pattern[slot] == kDense) {
+  const int pattern = a.pattern[slot];
+  if (pattern == kDense) {
     if (lane == 0) cnt[row] = a.nb;
     return;
   }
+  if (pattern == kStride) {  // token-level sampling: count of 64-key groups, no list
+    const int64_t keys = (a.n + a.param[slot] - 1) / a.param[slot];
+    if (lane == 0) cnt[row] = (int)((keys + kBlock - 1) / kBlock);
+    return;
+  }
   const int64_t T = a.tokens_per_frame;
-  const int64_t first = (int64_t)i * kBlock;
-  const int64_t last = min(first + kBlock, a.n) - 1;
-  const int64_t tok_lo = (first / T) * T;
-  const int64_t tok_hi = min((last / T + 1) * T, a.n) - 1;
+  int64_t tok_lo, tok_hi;  // token range whose blocks are kept
+  if (pattern == kAnchor) {
+    tok_lo = (int64_t)a.param[slot] * T;
+    tok_hi = min(tok_lo + T, a.n) - 1;
+  } else {  // frame-local: the frames touched by block i
+    const int64_t first = (int64_t)i * kBlock;
+    const int64_t last = min(first + kBlock, a.n) - 1;
+    tok_lo = (first / T) * T;
+    tok_hi = min((last / T + 1) * T, a.n) - 1;
+  }
   const int j_lo = (int)(tok_lo / kBlock);
   const int len = (int)(tok_hi / kBlock) - j_lo + 1;
   int32_t* dst = idx + row * a.cap;
   for (int p = lane; p < a.cap; p += 64) dst[p] = p < len ? j_lo + p : -1;
   if (lane == 0) cnt[row] = len;
+}
+
+constexpr int kGlobalThreads = 256;
+
+// One workgroup per global-probe head; writes row 0 of the head's lists.
+__global__ __launch_bounds__(kGlobalThreads) void select_global_kernel(const double* __restrict__ qp,
+                                                                      const double* __restrict__ kpT,
+                                                                      int32_t* __restrict__ idx,
+                                                                      int32_t* __restrict__ cnt,
+                                                                      double* __restrict__ scores,
+                                                                      GlobalArgs a) {
+  extern __shared__ __attribute__((aligned(16))) uint64_t skeys[];  // [nb] order keys
+  __shared__ double part[kGlobalThreads / 64][kHeadDim];
+  __shared__ double qbar[kHeadDim];
+  __shared__ uint32_t hist[256];
+  __shared__ uint32_t wave_tot[kGlobalThreads / 64][2];
+  __shared__ int sel_digit, sel_above;
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const int h = a.head[blockIdx.x];
+  const int k = a.topk[blockIdx.x];
+  const int nb = a.nb;
+  const double* qh = qp + (int64_t)h * nb * kHeadDim;
+  const double* kT = kpT + (int64_t)h * kHeadDim * nb;
+
+  // probe: mean of all queries = sum over blocks of (block size) * block mean, over N
+  double acc = 0.0;
+  for (int b = wave; b < nb; b += kGlobalThreads / 64) {
+    const double nbk = b == nb - 1 ? (double)(a.n - (int64_t)(nb - 1) * kBlock) : (double)kBlock;
+    acc = fma(nbk, qh[(int64_t)b * kHeadDim + lane], acc);
+  }
+  part[wave][lane] = acc;
+  __syncthreads();
+  if (t < kHeadDim) {
+    double sum = 0.0;
+#pragma unroll
+    for (int w = 0; w < kGlobalThreads / 64; ++w) sum += part[w][t];
+    qbar[t] = sum / (double)a.n;
+  }
+  __syncthreads();
+
+  // scores of every key block, in float64, kept as order keys
+  for (int j = t; j < nb; j += kGlobalThreads) {
+    double sj = 0.0;
+    for (int d = 0; d < kHeadDim; ++d) sj = fma(qbar[d], kT[(int64_t)d * nb + j], sj);
+    sj *= 0.125;  // 1/sqrt(64), exact
+    skeys[j] = order_key(sj);
+    if (scores) scores[(int64_t)h * nb * nb + j] = sj;
+  }
+  __syncthreads();
+
+  // k-th largest key, one 8-bit digit at a time from the top
+  uint64_t prefix = 0, mask = 0;
+  int remaining = k;
+  for (int shift = 56; shift >= 0; shift -= 8) {
+    hist[t] = 0;  // kGlobalThreads == 256 bins
+    __syncthreads();
+    for (int j = t; j < nb; j += kGlobalThreads) {
+      const uint64_t key = skeys[j];
+      if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255], 1u);
+    }
+    __syncthreads();
+    if (t == 0) {
+      int above = 0, d = 255;
+      for (; d > 0; --d) {
+        if (above + (int)hist[d] >= remaining) break;
+        above += (int)hist[d];
+      }
+      sel_digit = d;
+      sel_above = above;
+    }
+    __syncthreads();
+    prefix |= (uint64_t)sel_digit << shift;
+    mask |= 0xffull << shift;
+    remaining -= sel_above;
+    __syncthreads();
+  }
+  // prefix is the k-th largest key; keep keys above it and the `remaining`
+  // lowest-index keys equal to it, in ascending block order
+  int32_t* dst = idx + (int64_t)h * nb * a.cap;
+  int out_pos = 0, eq_seen = 0;
+  for (int j0 = 0; j0 < nb; j0 += kGlobalThreads) {
+    const int j = j0 + t;
+    const uint64_t key = j < nb ? skeys[j] : 0ull;
+    const bool gt = j < nb && key > prefix;
+    const bool eq = j < nb && key == prefix;
+    const uint64_t below = (1ull << lane) - 1;
+    const uint64_t eq_mask = __ballot(eq);
+    if (lane == 0) wave_tot[wave][0] = (uint32_t)__popcll(eq_mask);
+    __syncthreads();
+    int eq_before = eq_seen + __popcll(eq_mask & below);
+    for (int w = 0; w < wave; ++w) eq_before += (int)wave_tot[w][0];
+    const bool kept = gt || (eq && eq_before < remaining);
+    const uint64_t kept_mask = __ballot(kept);
+    if (lane == 0) wave_tot[wave][1] = (uint32_t)__popcll(kept_mask);
+    __syncthreads();
+    int pos = out_pos + __popcll(kept_mask & below);
+    for (int w = 0; w < wave; ++w) pos += (int)wave_tot[w][1];
+    if (kept && pos < a.cap) dst[pos] = j;
+    int eq_chunk = 0, kept_chunk = 0;
+#pragma unroll
+    for (int w = 0; w < kGlobalThreads / 64; ++w) {
+      eq_chunk += (int)wave_tot[w][0];
+      kept_chunk += (int)wave_tot[w][1];
+    }
+    eq_seen += eq_chunk;
+    out_pos += kept_chunk;
+    __syncthreads();
+  }
+  for (int p = out_pos + t; p < a.cap; p += kGlobalThreads) dst[p] = -1;
+  if (t == 0) cnt[(int64_t)h * nb] = out_pos;
+}
+
+// Copies row 0 of every global-probe head to its other query blocks: one
+// wave per (head, row >= 1).
+__global__ __launch_bounds__(256) void select_global_broadcast_kernel(int32_t* __restrict__ idx,
+                                                                    int32_t* __restrict__ cnt,
+                                                                    GlobalArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int64_t wave = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int64_t rows = (int64_t)a.n_heads * (a.nb - 1);
+  if (wave >= rows) return;
+  const int slot = (int)(wave / (a.nb - 1));
+  const int i = 1 + (int)(wave - (int64_t)slot * (a.nb - 1));
+  const int h = a.head[slot];
+  const int32_t* src = idx + (int64_t)h * a.nb * a.cap;
+  int32_t* dst = idx + ((int64_t)h * a.nb + i) * a.cap;
+  for (int p = lane; p < a.cap; p += 64) dst[p] = src[p];
+  if (lane == 0) cnt[(int64_t)h * a.nb + i] = cnt[(int64_t)h * a.nb];
 }
 
 template <int R, int THREADS, int MAXK>
@@ -552,6 +702,23 @@ hipError_t launch_select_topk(const double* qp, const double* kpT, int32_t* idx,
     case 1: return launch_topk_rows<1, 256>(qp, kpT, idx, cnt, scores, a, lds, s);
     default: return hipErrorInvalidValue;
   }
+}
+
+hipError_t launch_select_global(const double* qp, const double* kpT, int32_t* idx, int32_t* cnt,
+                                double* scores, const GlobalArgs& a, hipStream_t s) {
+  if (a.n_heads == 0) return hipSuccess;
+  const size_t lds = (size_t)a.nb * sizeof(uint64_t);
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(select_global_kernel),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(select_global_kernel, dim3((unsigned)a.n_heads), dim3(kGlobalThreads), lds, s,
+                     qp, kpT, idx, cnt, scores, a);
+  e = hipGetLastError();
+  if (e != hipSuccess || a.nb == 1) return e;
+  const int64_t waves = (int64_t)a.n_heads * (a.nb - 1);
+  hipLaunchKernelGGL(select_global_broadcast_kernel, dim3((unsigned)((waves + 3) / 4)), dim3(256),
+                     0, s, idx, cnt, a);
+  return hipGetLastError();
 }
 
 hipError_t launch_select_static(int32_t* idx, int32_t* cnt, const StaticArgs& a, hipStream_t s) {

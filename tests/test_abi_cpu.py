@@ -70,12 +70,41 @@ def test_table_validation_and_capacity(B):
     assert cap(ctypes.byref(p), B.head_table([(0, 0)] * 3)) == 1
     assert cap(ctypes.byref(p), B.head_table([(0, 0), (2, 0), (2, 1)])) == -5
     assert cap(ctypes.byref(p), B.head_table([(0, 0), (2, 173), (2, 1)])) == -5
-    assert cap(ctypes.byref(p), B.head_table([(0, 0), (3, 1), (2, 1)])) == -5
+    assert cap(ctypes.byref(p), B.head_table([(0, 0), (6, 1), (2, 1)])) == -5  # unknown class
+    assert cap(ctypes.byref(p), B.head_table([(0, 0), (-1, 1), (2, 1)])) == -5
     assert cap(ctypes.byref(p), None) == -1
     # frames of 128 tokens align with blocks: two blocks per frame
     assert cap(ctypes.byref(_p(B, heads=1, frames=4, T=128)), B.head_table([(1, 0)])) == 2
     # one 300-token frame: every block shares it
     assert cap(ctypes.byref(_p(B, heads=1, frames=1, T=300)), B.head_table([(1, 0)])) == 5
+
+
+def test_new_classes_validation_and_capacity(B):
+    lib = B.load()
+    cap = lib.saf3r_index_capacity
+    p = _p(B, heads=2, frames=8, T=1374)  # N = 10992, nb = 172
+    # ANCHOR: frame index in [0, frames); frame 0 = tokens 0..1373 -> blocks 0..21;
+    # frame 3 = tokens 4122..5495 -> blocks 64..85
+    assert cap(ctypes.byref(p), B.head_table([(B.ANCHOR, 0), (0, 0)])) == 22
+    assert cap(ctypes.byref(p), B.head_table([(B.ANCHOR, 3), (0, 0)])) == 22
+    assert cap(ctypes.byref(p), B.head_table([(B.ANCHOR, 7), (0, 0)])) == 22
+    assert cap(ctypes.byref(p), B.head_table([(B.ANCHOR, 8), (0, 0)])) == -5
+    assert cap(ctypes.byref(p), B.head_table([(B.ANCHOR, -1), (0, 0)])) == -5
+    # STRIDE: key stride in [1, N]; no list
+    assert cap(ctypes.byref(p), B.head_table([(B.STRIDE, 64), (0, 0)])) == 1
+    assert cap(ctypes.byref(p), B.head_table([(B.STRIDE, 10992), (0, 0)])) == 1
+    assert cap(ctypes.byref(p), B.head_table([(B.STRIDE, 0), (0, 0)])) == -5
+    assert cap(ctypes.byref(p), B.head_table([(B.STRIDE, 10993), (0, 0)])) == -5
+    # GLOBAL_PROBE: kept blocks in [1, nb]
+    assert cap(ctypes.byref(p), B.head_table([(B.GLOBAL_PROBE, 40), (2, 7)])) == 40
+    assert cap(ctypes.byref(p), B.head_table([(B.GLOBAL_PROBE, 172), (0, 0)])) == 172
+    assert cap(ctypes.byref(p), B.head_table([(B.GLOBAL_PROBE, 173), (0, 0)])) == -5
+    assert cap(ctypes.byref(p), B.head_table([(B.GLOBAL_PROBE, 0), (0, 0)])) == -5
+    # a table of DENSE and STRIDE heads needs no lists: attention accepts null lists
+    fake = ctypes.c_void_p(0x1000)
+    t = B.head_table([(B.STRIDE, 4), (0, 0)])
+    assert lib.saf3r_sparse_attention(ctypes.byref(p), t, fake, fake, fake, None, None, 0,
+                                      None, None, None) == -1  # out missing, lists not required
 
 
 def test_calls_reject_bad_arguments_before_launch(B):

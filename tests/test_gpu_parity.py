@@ -18,6 +18,10 @@ def _tols(w):
     return (PT.TOL_BF16, PT.LSE_TOL_BF16) if w.dtype == "bf16" else (PT.TOL_F32, PT.LSE_TOL_F32)
 
 
+def _stride_blocks(n, stride):
+    return -(-(-(-n // stride)) // 64)
+
+
 def _full_check(P, w, q, k, v, table, want_scores=True):
     res = PT.gpu_layer(P, w, q, k, v, table, want_scores=want_scores)
     ref = O.run_layer(q, k, v, table, w.tokens_per_frame, w.dtype)
@@ -25,19 +29,24 @@ def _full_check(P, w, q, k, v, table, want_scores=True):
     nb = w.nb
     cap = res["idx"].shape[2]
     near = 0
-    for h, (pattern, _) in enumerate(table):
-        if pattern == O.TOPK:
+    for h, (pattern, param) in enumerate(table):
+        if pattern in (O.TOPK, O.GLOBAL_PROBE):
             # pooled means: exact sums of bf16 in fp64, division correctly rounded
             np.testing.assert_allclose(res["q_pooled"][h], ref["q_pooled"][h], rtol=1e-15, atol=0)
             np.testing.assert_allclose(res["k_pooled"][h], ref["k_pooled"][h], rtol=1e-15, atol=0)
-            if want_scores:
+            if want_scores and pattern == O.TOPK:
                 np.testing.assert_allclose(res["scores"][h], ref["scores"][h], rtol=1e-12, atol=1e-13)
-        for i in range(nb):
-            status = PT.check_lists(res, h, i, pattern, ref["lists"][h][i], ref["margins"][h][i], nb, cap)
-            near += status == "near_tie"
+            if want_scores and pattern == O.GLOBAL_PROBE:  # probe scores in row 0
+                np.testing.assert_allclose(res["scores"][h][0], ref["scores"][h], rtol=1e-12, atol=1e-13)
+        if pattern == O.STRIDE:
+            assert np.all(res["cnt"][h] == _stride_blocks(w.tokens, param)), f"head {h}: stride count"
+        else:
+            for i in range(nb):
+                status = PT.check_lists(res, h, i, pattern, ref["lists"][h][i], ref["margins"][h][i], nb, cap)
+                near += status == "near_tie"
         out_ref, lse_ref = ref["out"][h], ref["lse"][h]
-        if near:
-            lists = [PT.gpu_list(res, h, i) if pattern != O.DENSE else np.arange(nb) for i in range(nb)]
+        if near and pattern not in (O.DENSE, O.STRIDE):
+            lists = [PT.gpu_list(res, h, i) for i in range(nb)]
             qh, kh, vh = (O.to_f64(x[h], w.dtype) for x in (q, k, v))
             out_ref, lse_ref = O.attend_head(qh, kh, vh, lists, 64)
         err = PT.max_abs(res["out"][h], out_ref)
@@ -188,3 +197,77 @@ def test_all_dense_table_is_the_dense_baseline(gpu_lib):
         o_ref, l_ref = O.dense_attention(*(O.to_f64(x[h], "bf16") for x in (q, k, v)))
         assert PT.max_abs(out[h], o_ref) <= PT.TOL_BF16
         assert PT.max_abs(lse[h].cpu().numpy().astype(np.float64), l_ref) <= PT.LSE_TOL_BF16
+
+
+# ------------------------------------------ anchor, stride, global probe
+
+
+def _all_classes_table(w):
+    nb, n = w.nb, w.tokens
+    return [(O.DENSE, 0), (O.FRAME_LOCAL, 0), (O.TOPK, max(1, nb // 8)), (O.ANCHOR, 0),
+            (O.ANCHOR, w.frames - 1), (O.STRIDE, 1), (O.STRIDE, 2), (O.STRIDE, 7),
+            (O.STRIDE, min(64, n)), (O.STRIDE, max(1, n - 1)), (O.GLOBAL_PROBE, max(1, nb // 4)),
+            (O.GLOBAL_PROBE, nb)]
+
+
+@pytest.mark.parametrize("frames,T,dtype", [(4, 261, "f32"), (8, 1374, "bf16"), (3, 100, "bf16"),
+                                            (1, 129, "bf16"), (2, 20, "f32")])
+def test_all_classes_full_parity(gpu_lib, frames, T, dtype):
+    import paper_2607_03612_amd as P
+
+    w = Workload(f"classes-{frames}x{T}-{dtype}", frames, T, dtype, ("fixed", 1, 1, 50), heads=12)
+    q, k, v = make_qkv(w)
+    table = _all_classes_table(w)
+    print(f"[parity] all classes {w.name} nb={w.nb} table={table}", flush=True)
+    _, _, near = _full_check(P, w, q, k, v, table)
+    print(f"[parity] {w.name}: near-ties {near}", flush=True)
+
+
+def test_stride_one_equals_dense_bitwise(gpu_lib):
+    import paper_2607_03612_amd as P
+
+    w = Workload("stride-eq-dense", 3, 261, "bf16", ("fixed", 1, 1, 50), heads=2)
+    q, k, v = make_qkv(w)
+    for x in (q, k, v):
+        x[1] = x[0]
+    a = PT.gpu_layer(P, w, q, k, v, [(O.DENSE, 0), (O.STRIDE, 1)])
+    np.testing.assert_array_equal(a["out"][0], a["out"][1])
+    np.testing.assert_array_equal(a["lse"][0], a["lse"][1])
+
+
+def test_global_probe_gives_every_query_block_one_list(gpu_lib):
+    import paper_2607_03612_amd as P
+
+    w = WORKLOADS["S32xT1374-bf16"]
+    q, k, v = make_qkv(w)
+    table = [(O.GLOBAL_PROBE, 69)] + [(O.DENSE, 0)] * 15
+    res = PT.gpu_layer(P, w, q, k, v, table, want_lse=False)
+    rows = res["idx"][0, :, :int(res["cnt"][0, 0])]
+    assert np.all(res["cnt"][0] == 69) and np.all(rows == rows[0])
+    qh, kh = O.to_f64(q[0], "bf16"), O.to_f64(k[0], "bf16")
+    sel, margin, _ = O.global_probe_row(qh, kh, 69, 64)
+    if margin > PT.NEAR_TIE:
+        np.testing.assert_array_equal(rows[0], sel)
+
+
+@pytest.mark.parametrize("stride", [8, 33])
+def test_stride_sampled_parity_large(gpu_lib, stride):
+    """The 137400-token layer with STRIDE heads, checked on sampled query
+    blocks against the oracle's strided attention."""
+    import paper_2607_03612_amd as P
+
+    w = WORKLOADS["S100xT1374-bf16"]
+    q, k, v = make_qkv(w)
+    table = [(O.STRIDE, stride)] * 2 + [(O.DENSE, 0)] * 14
+    tq, tk, tv = (PT.to_device(x, "bf16") for x in (q, k, v))
+    out, lse = P.sparse_attention(tq, tk, tv, table, w.frames, w.tokens_per_frame, want_lse=True)
+    out = PT.out_to_numpy(out)
+    lse = lse.cpu().numpy().astype(np.float64)
+    keys = O.stride_keys(w.tokens, stride)
+    for h in range(2):
+        qh, kh, vh = (O.to_f64(x[h], "bf16") for x in (q, k, v))
+        for i in PT.sample_blocks(w.nb, 12, stride + h):
+            r = O.block_range(i, w.tokens, 64)
+            o_ref, l_ref = O.attend_tokens(qh, kh, vh, r, keys)
+            assert PT.max_abs(out[h][r.start:r.stop], o_ref) <= PT.TOL_BF16, (h, i)
+            assert PT.max_abs(lse[h][r.start:r.stop], l_ref) <= PT.LSE_TOL_BF16, (h, i)
