@@ -70,7 +70,12 @@ typedef enum { SAF3R_F32 = 0, SAF3R_BF16 = 1 } saf3r_dtype;
  *                       per head, the mean qbar of all N queries; keep the
  *                       param key blocks with the largest qbar . kbar_j / 8,
  *                       ties to the lower j, the same list for every query
- *                       block; param in [1, nb].
+ *                       block; param in [1, nb];
+ *   SAF3R_COSINE_TOPK   DINO Top-K kernel, block-wise (Sec. 4.1, 4.3): per
+ *                       frame, the param key blocks whose caller-supplied
+ *                       features are most similar to the query block's;
+ *                       param in [1, 64]. Lists come from
+ *                       saf3r_cosine_select, once per sequence.
  */
 typedef enum {
   SAF3R_DENSE = 0,
@@ -78,7 +83,8 @@ typedef enum {
   SAF3R_TOPK = 2,
   SAF3R_ANCHOR = 3,
   SAF3R_STRIDE = 4,
-  SAF3R_GLOBAL_PROBE = 5
+  SAF3R_GLOBAL_PROBE = 5,
+  SAF3R_COSINE_TOPK = 6
 } saf3r_pattern;
 
 typedef struct {
@@ -98,10 +104,10 @@ typedef struct {
 /* Number of 64-token blocks, ceil(N / 64), or a negative saf3r_status. */
 int32_t saf3r_num_blocks(const saf3r_problem* problem);
 
-/* Smallest `cap` accepted by saf3r_select_blocks / saf3r_sparse_attention:
- * the longest kept-block list of any FRAME_LOCAL, TOPK, ANCHOR or
- * GLOBAL_PROBE head (at least 1), or a negative saf3r_status. DENSE and
- * STRIDE heads need no list. */
+/* Smallest `cap` accepted by saf3r_select_blocks / saf3r_cosine_select /
+ * saf3r_sparse_attention: the longest kept-block list of any FRAME_LOCAL,
+ * TOPK, ANCHOR, GLOBAL_PROBE or COSINE_TOPK head (at least 1), or a negative
+ * saf3r_status. DENSE and STRIDE heads need no list. */
 int32_t saf3r_index_capacity(const saf3r_problem* problem, const saf3r_head_cfg* table);
 
 /* Block pooling (Sec. 4.3: the probe of a set of queries is their mean).
@@ -132,7 +138,9 @@ saf3r_status saf3r_estimate_blocks(const saf3r_problem* problem, const saf3r_hea
  *                 64-key groups of the sampled keys; block_idx untouched;
  *   GLOBAL_PROBE: the param highest probe scores qbar . kbar_j / 8 with qbar
  *                 the mean of all N queries (float64), ties to the lower j,
- *                 the same list in every row i.
+ *                 the same list in every row i;
+ *   COSINE_TOPK:  block_idx and block_cnt left untouched (their lists come
+ *                 from saf3r_cosine_select and stay valid across layers).
  * Lists are written ascending, padded with -1 up to cap.
  *   q_pooled, k_pooled device float64, [heads, nb, 64] and [heads, 64, nb], as
  *                      written by saf3r_estimate_blocks (read for TOPK and
@@ -173,6 +181,33 @@ saf3r_status saf3r_sparse_attention(const saf3r_problem* problem, const saf3r_he
                                     const void* q, const void* k, const void* v,
                                     const int32_t* block_idx, const int32_t* block_cnt, int32_t cap,
                                     void* out, float* lse_or_null, void* stream);
+
+/* Workspace bytes saf3r_cosine_select needs for features of width
+ * feat_dim: (feat_dim * nb + nb * nb) * 8, or a negative saf3r_status. */
+int64_t saf3r_cosine_workspace_bytes(const saf3r_problem* problem, int32_t feat_dim);
+
+/* Per-frame cosine Top-K lists of every COSINE_TOPK head (the DINO Top-K
+ * kernel of Sec. 4.1, block-wise variant of Sec. 4.3). Each token's feature
+ * is scaled to unit length and averaged over its block (float64); the block
+ * similarity sim[i][j] = fbar_i . fbar_j is the mean cosine similarity over
+ * the tile of token pairs. For head h (param k) and query block i the kept
+ * blocks are, for every frame f, the min(k, |B_f|) blocks j of
+ * B_f = { j : floor(64 j / tokens_per_frame) = f } with the largest sim[i][j]
+ * (ties to the lower j), written ascending and padded with -1. The lists
+ * depend on the features only: the paper computes them once per sequence
+ * and reuses them in every layer, and saf3r_select_blocks leaves these rows
+ * untouched so a caller can do the same.
+ *   features         device [N, feat_dim] of problem->dtype; every row non-zero
+ *   feat_dim         1 .. 4096
+ *   workspace        device, >= saf3r_cosine_workspace_bytes bytes, 8-byte
+ *                    aligned; overwritten (block features, similarity matrix)
+ *   block_idx, block_cnt, cap   as for saf3r_select_blocks; only rows of
+ *                    COSINE_TOPK heads are written
+ * Returns SAF3R_OK, or an error with nothing enqueued. */
+saf3r_status saf3r_cosine_select(const saf3r_problem* problem, const saf3r_head_cfg* table,
+                                 const void* features, int32_t feat_dim, void* workspace,
+                                 int64_t workspace_bytes, int32_t* block_idx, int32_t* block_cnt,
+                                 int32_t cap, void* stream);
 
 /* Static description of a status code (never NULL). */
 const char* saf3r_status_string(int32_t status);

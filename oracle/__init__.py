@@ -12,12 +12,16 @@ from .saf3r_oracle import (  # noqa: F401
     STRIDE,
     TOPK,
     anchor_row,
+    COSINE_TOPK,
     attend_block,
     attend_head,
     attend_stride,
     attend_tokens,
     block_range,
+    block_frame,
     block_scores,
+    cosine_block_features,
+    cosine_topk_row,
     dense_attention,
     frame_local_row,
     global_probe_row,

@@ -24,7 +24,9 @@ fusion or reordering beyond what the definitions state:
    lower block index, GLOBAL_PROBE (the query-probe kernel as Sec. 4.3 states
    it) ranks key blocks by the single mean query of the whole sequence and
    gives every query block the same ``k`` blocks, STRIDE (the uniform sampling
-   kernel) keeps every ``s``-th key token.
+   kernel) keeps every ``s``-th key token, COSINE_TOPK (the DINO Top-K kernel,
+   block-wise, on caller-supplied features) keeps per frame the ``k`` key
+   blocks whose features are most similar to the query block's.
 4. Attention restricted to the kept keys (Sec. 4.1, Query-Probe Top-K kernel):
    softmax over the kept key tokens, renormalised over that set, times V.
 5. NMSE (Sec. 4.2, Eq. 1) between full and sparse outputs, as a quality
@@ -33,6 +35,9 @@ fusion or reordering beyond what the definitions state:
 Pins (checked by the CPU tests, not by this module): pooling+scores against
 the brute-force tile mean of S; Top-K against brute force over all k-subsets;
 frame-local and anchor lists against hand-worked examples and token loops;
+the cosine block similarity against the brute-force tile mean of token
+cosine similarities and the per-frame selection against per-frame subset
+enumeration;
 the global probe against the column mean of the full S computed by brute
 force (the identity of Sec. 4.3); attention (block lists and strided keys)
 against a library softmax attention with an explicit token mask; NMSE
@@ -50,6 +55,7 @@ TOPK = 2
 ANCHOR = 3
 STRIDE = 4
 GLOBAL_PROBE = 5
+COSINE_TOPK = 6
 
 
 # --------------------------------------------------------------------------
@@ -155,6 +161,39 @@ def global_probe_row(q_head: np.ndarray, k_head: np.ndarray, k: int, block: int)
     return sel, margin, s
 
 
+def cosine_block_features(f: np.ndarray, block: int) -> np.ndarray:
+    """Block-wise feature for the DINO Top-K kernel (Sec. 4.3, block-wise
+    variant): every token's feature scaled to unit length, then averaged over
+    the block. The dot product of two such means is the mean cosine
+    similarity over the (query block, key block) tile of token pairs."""
+    norms = np.sqrt(np.sum(f * f, axis=1, keepdims=True))
+    return pool_blocks(f / norms, block)
+
+
+def block_frame(j: int, tokens_per_frame: int, block: int) -> int:
+    """Frame a key block is counted under for per-frame selection: the frame
+    of its first token."""
+    return (j * block) // tokens_per_frame
+
+
+def cosine_topk_row(sim_row: np.ndarray, k: int, tokens_per_frame: int, block: int):
+    """Per-frame Top-K (Sec. 4.1, DINO Top-K: the most similar keys from each
+    frame): for every frame, the ``k`` key blocks of that frame with the
+    highest similarity (ties to the lower index; all of the frame's blocks if
+    it has at most ``k``). Returns (ascending indices, margin) where the
+    margin is the smallest gap, over frames that drop a block, between the
+    k-th and (k+1)-th ranked similarities."""
+    nb = sim_row.shape[0]
+    frame = np.array([block_frame(j, tokens_per_frame, block) for j in range(nb)])
+    kept, margin = [], math.inf
+    for f in np.unique(frame):
+        js = np.nonzero(frame == f)[0]
+        sel, m = topk_row(sim_row[js], min(k, len(js)))
+        kept.extend(js[sel].tolist())
+        margin = min(margin, m)
+    return np.array(sorted(kept), dtype=np.int64), margin
+
+
 def stride_keys(n: int, stride: int) -> np.ndarray:
     """Key tokens kept by the uniform sampling kernel (Sec. 4.1): every
     ``stride``-th token, starting at token 0."""
@@ -164,11 +203,13 @@ def stride_keys(n: int, stride: int) -> np.ndarray:
 
 
 def select_head(pattern: int, topk: int, q_head: np.ndarray, k_head: np.ndarray,
-                tokens_per_frame: int, block: int):
+                tokens_per_frame: int, block: int, features: np.ndarray = None):
     """Kept key blocks of every query block of one head.
 
     ``topk`` is the class parameter: the kept block count (TOPK,
-    GLOBAL_PROBE), the anchor frame (ANCHOR) or the key stride (STRIDE).
+    GLOBAL_PROBE), the anchor frame (ANCHOR), the key stride (STRIDE) or the
+    blocks kept per frame (COSINE_TOPK, which also takes the per-token
+    ``features``).
     Returns (lists, margins, scores): ``lists[i]`` ascending int64 (None for
     STRIDE, which keeps tokens, not blocks), ``margins`` the Top-K margins
     (+inf for the other classes), ``scores`` the block score matrix of a TOPK
@@ -201,6 +242,16 @@ def select_head(pattern: int, topk: int, q_head: np.ndarray, k_head: np.ndarray,
         sel, margin, s = global_probe_row(q_head, k_head, topk, block)
         margins[:] = margin
         return [sel for _ in range(nb)], margins, s
+    if pattern == COSINE_TOPK:
+        if topk < 1 or features is None:
+            raise ValueError("cosine top-k needs k >= 1 and features")
+        fb = cosine_block_features(features, block)
+        sim = fb @ fb.T
+        lists = []
+        for i in range(nb):
+            sel, margins[i] = cosine_topk_row(sim[i], topk, tokens_per_frame, block)
+            lists.append(sel)
+        return lists, margins, sim
     if pattern == STRIDE:
         # token-level: no block list; attention uses stride_keys
         if not 1 <= topk <= n:
@@ -295,12 +346,14 @@ def kept_fraction(lists_per_head, nb: int) -> float:
 
 
 def run_layer(q, k, v, table, tokens_per_frame: int, dtype: str, block: int = 64,
-              heads=None, with_attention: bool = True):
+              heads=None, with_attention: bool = True, features=None):
     """The whole hot path for one layer.
 
     ``q, k, v``: ``[H, N, D]`` fp32 arrays or bf16 bit patterns; ``table``:
-    per-head ``(pattern, topk)``. Returns a dict with per-head lists, margins,
-    pooled vectors (Top-K heads), scores, outputs and log-sum-exps (float64)."""
+    per-head ``(pattern, param)``; ``features``: per-token features ``[N, Df]``
+    (float64) for COSINE_TOPK heads. Returns a dict with per-head lists,
+    margins, pooled vectors (Top-K heads), scores, outputs and log-sum-exps
+    (float64)."""
     H = q.shape[0]
     heads = range(H) if heads is None else heads
     res = {"lists": {}, "margins": {}, "scores": {}, "q_pooled": {}, "k_pooled": {},
@@ -308,7 +361,7 @@ def run_layer(q, k, v, table, tokens_per_frame: int, dtype: str, block: int = 64
     for h in heads:
         pattern, topk = table[h]
         qh, kh = to_f64(q[h], dtype), to_f64(k[h], dtype)
-        lists, margins, s = select_head(pattern, topk, qh, kh, tokens_per_frame, block)
+        lists, margins, s = select_head(pattern, topk, qh, kh, tokens_per_frame, block, features)
         res["lists"][h], res["margins"][h], res["scores"][h] = lists, margins, s
         if pattern in (TOPK, GLOBAL_PROBE):
             res["q_pooled"][h] = pool_blocks(qh, block)

@@ -7,12 +7,15 @@ from . import binding  # noqa: F401
 from .binding import (  # noqa: F401
     ANCHOR,
     BF16,
+    COSINE_TOPK,
     DENSE,
     F32,
     FRAME_LOCAL,
     GLOBAL_PROBE,
     TOPK,
     Saf3rError,
+    cosine_select,
+    cosine_workspace_bytes,
     estimate_blocks,
     index_capacity,
     load,

@@ -13,7 +13,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG, "libsaf3r.so")
 
 F32, BF16 = 0, 1
-DENSE, FRAME_LOCAL, TOPK, ANCHOR, STRIDE, GLOBAL_PROBE = 0, 1, 2, 3, 4, 5
+DENSE, FRAME_LOCAL, TOPK, ANCHOR, STRIDE, GLOBAL_PROBE, COSINE_TOPK = 0, 1, 2, 3, 4, 5, 6
 HEAD_DIM = 64
 BLOCK = 64
 
@@ -23,6 +23,8 @@ EXPORTS = (
     "saf3r_estimate_blocks",
     "saf3r_select_blocks",
     "saf3r_sparse_attention",
+    "saf3r_cosine_workspace_bytes",
+    "saf3r_cosine_select",
     "saf3r_status_string",
 )
 
@@ -58,6 +60,10 @@ def _declare(lib):
     lib.saf3r_select_blocks.restype = I32
     lib.saf3r_sparse_attention.argtypes = [P, C, V, V, V, V, V, I32, V, V, V]
     lib.saf3r_sparse_attention.restype = I32
+    lib.saf3r_cosine_workspace_bytes.argtypes = [P, I32]
+    lib.saf3r_cosine_workspace_bytes.restype = ctypes.c_int64
+    lib.saf3r_cosine_select.argtypes = [P, C, V, I32, V, ctypes.c_int64, V, V, I32, V]
+    lib.saf3r_cosine_select.restype = I32
     lib.saf3r_status_string.argtypes = [I32]
     lib.saf3r_status_string.restype = ctypes.c_char_p
 
@@ -210,6 +216,39 @@ def sparse_attention(q, k, v, table, frames, tokens_per_frame, block_idx=None, b
                                          _ptr(lse), _stream(stream)),
            "saf3r_sparse_attention")
     return out, lse
+
+
+def cosine_workspace_bytes(frames, tokens_per_frame, feat_dim, heads=1, dtype=BF16) -> int:
+    p = problem(heads, frames, tokens_per_frame, dtype)
+    r = _lib().saf3r_cosine_workspace_bytes(ctypes.byref(p), int(feat_dim))
+    _check(min(r, 0), "saf3r_cosine_workspace_bytes")
+    return int(r)
+
+
+def cosine_select(features, table, frames, tokens_per_frame, block_idx, block_cnt, workspace=None,
+                  stream=None):
+    """Per-frame cosine Top-K lists of the COSINE_TOPK heads, written into
+    ``block_idx [H, nb, cap]`` / ``block_cnt [H, nb]`` (other heads' rows
+    untouched). ``features``: device ``[N, feat_dim]`` of the layer dtype."""
+    import torch
+
+    if not (features.is_cuda and features.is_contiguous() and features.dim() == 2):
+        raise ValueError("features must be a contiguous device tensor [N, feat_dim]")
+    N, D = features.shape
+    if frames * tokens_per_frame != N:
+        raise ValueError("frames * tokens_per_frame must equal the feature rows")
+    code = _torch_dtype_code(features)
+    H = len(table)
+    nbytes = cosine_workspace_bytes(frames, tokens_per_frame, D, H, code)
+    if workspace is None:
+        workspace = torch.empty(nbytes // 8, dtype=torch.float64, device=features.device)
+    p = problem(H, frames, tokens_per_frame, code)
+    _check(_lib().saf3r_cosine_select(ctypes.byref(p), head_table(table), _ptr(features), int(D),
+                                      _ptr(workspace), int(workspace.numel() * workspace.element_size()),
+                                      _ptr(block_idx), _ptr(block_cnt), int(block_idx.shape[2]),
+                                      _stream(stream)),
+           "saf3r_cosine_select")
+    return block_idx, block_cnt
 
 
 def run_layer(q, k, v, table, frames, tokens_per_frame, stream=None):

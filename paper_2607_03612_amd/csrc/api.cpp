@@ -63,6 +63,9 @@ saf3r_status check_table(const Shape& s, const saf3r_head_cfg* t) {
       case SAF3R_STRIDE:
         if (p < 1 || (int64_t)p > s.n) return SAF3R_ERR_BAD_TABLE;
         break;
+      case SAF3R_COSINE_TOPK:
+        if (p < 1 || p > saf3r::kMaxCosinePerFrame) return SAF3R_ERR_BAD_TABLE;
+        break;
       default:
         return SAF3R_ERR_BAD_TABLE;
     }
@@ -94,6 +97,19 @@ int anchor_len(const Shape& s, int a) {
   return (int)(hi / saf3r::kBlock - lo / saf3r::kBlock + 1);
 }
 
+// Kept blocks of a COSINE_TOPK head keeping k per frame (a key block counts
+// under the frame of its first token): sum over frames of min(k, blocks).
+int cosine_len(const Shape& s, int k) {
+  const int64_t T = s.tokens_per_frame;
+  int total = 0;
+  for (int64_t f = 0; f * T < s.n; ++f) {
+    const int64_t lo = (f * T + saf3r::kBlock - 1) / saf3r::kBlock;
+    const int64_t hi = std::min<int64_t>(((f + 1) * T + saf3r::kBlock - 1) / saf3r::kBlock, s.nb);
+    if (hi > lo) total += (int)std::min<int64_t>(k, hi - lo);
+  }
+  return total;
+}
+
 int capacity(const Shape& s, const saf3r_head_cfg* t) {
   int cap = 1;
   bool any_fl = false;
@@ -101,6 +117,7 @@ int capacity(const Shape& s, const saf3r_head_cfg* t) {
     const int p = t[h].pattern;
     if (p == SAF3R_TOPK || p == SAF3R_GLOBAL_PROBE) cap = std::max(cap, t[h].param);
     if (p == SAF3R_ANCHOR) cap = std::max(cap, anchor_len(s, t[h].param));
+    if (p == SAF3R_COSINE_TOPK) cap = std::max(cap, cosine_len(s, t[h].param));
     if (p == SAF3R_FRAME_LOCAL) any_fl = true;
   }
   if (any_fl) cap = std::max(cap, max_frame_local_len(s));
@@ -180,6 +197,8 @@ saf3r_status saf3r_select_blocks(const saf3r_problem* problem, const saf3r_head_
     } else if (table[h].pattern == SAF3R_GLOBAL_PROBE) {
       ga.head[ga.n_heads] = (int16_t)h;
       ga.topk[ga.n_heads++] = table[h].param;
+    } else if (table[h].pattern == SAF3R_COSINE_TOPK) {
+      // lists come from saf3r_cosine_select and are left as they are
     } else {
       sa.head[sa.n_heads] = (int16_t)h;
       sa.pattern[sa.n_heads] = (int8_t)table[h].pattern;
@@ -247,6 +266,7 @@ saf3r_status saf3r_sparse_attention(const saf3r_problem* problem, const saf3r_he
       case SAF3R_DENSE: cost[h] = s.nb; break;
       case SAF3R_FRAME_LOCAL: cost[h] = fl_len; break;
       case SAF3R_ANCHOR: cost[h] = anchor_len(s, table[h].param); break;
+      case SAF3R_COSINE_TOPK: cost[h] = cosine_len(s, table[h].param); break;
       case SAF3R_STRIDE:
         cost[h] = (int)((((s.n + table[h].param - 1) / table[h].param) + saf3r::kBlock - 1) / saf3r::kBlock);
         break;
@@ -275,6 +295,45 @@ saf3r_status saf3r_sparse_attention(const saf3r_problem* problem, const saf3r_he
   if (e != hipSuccess) return SAF3R_ERR_HIP;
   return hip_status(saf3r::launch_attention(s.dtype, q, k, v, block_idx, block_cnt, out,
                                             lse_or_null, sa, hs));
+}
+
+int64_t saf3r_cosine_workspace_bytes(const saf3r_problem* problem, int32_t feat_dim) {
+  Shape s;
+  const saf3r_status st = check_problem(problem, &s);
+  if (st != SAF3R_OK) return st;
+  if (feat_dim < 1 || feat_dim > saf3r::kMaxCosineDim) return SAF3R_ERR_INVALID_ARGUMENT;
+  return ((int64_t)feat_dim * s.nb + (int64_t)s.nb * s.nb) * (int64_t)sizeof(double);
+}
+
+saf3r_status saf3r_cosine_select(const saf3r_problem* problem, const saf3r_head_cfg* table,
+                                 const void* features, int32_t feat_dim, void* workspace,
+                                 int64_t workspace_bytes, int32_t* block_idx, int32_t* block_cnt,
+                                 int32_t cap, void* stream) {
+  Shape s;
+  saf3r_status st = check_problem(problem, &s);
+  if (st != SAF3R_OK) return st;
+  st = check_table(s, table);
+  if (st != SAF3R_OK) return st;
+  if (!features || !workspace || !block_idx || !block_cnt) return SAF3R_ERR_INVALID_ARGUMENT;
+  if (feat_dim < 1 || feat_dim > saf3r::kMaxCosineDim) return SAF3R_ERR_INVALID_ARGUMENT;
+  const int64_t need = saf3r_cosine_workspace_bytes(problem, feat_dim);
+  if (workspace_bytes < need) return SAF3R_ERR_CAPACITY;
+  if (cap < capacity(s, table)) return SAF3R_ERR_CAPACITY;
+  saf3r::CosineArgs a{};
+  a.n = s.n;
+  a.nb = s.nb;
+  a.cap = cap;
+  a.dim = feat_dim;
+  a.tokens_per_frame = s.tokens_per_frame;
+  for (int h = 0; h < s.heads; ++h) {
+    if (table[h].pattern != SAF3R_COSINE_TOPK) continue;
+    a.head[a.n_heads] = (int16_t)h;
+    a.topk[a.n_heads++] = table[h].param;
+  }
+  double* fb = static_cast<double*>(workspace);
+  double* sim = fb + (int64_t)feat_dim * s.nb;
+  return hip_status(saf3r::launch_cosine(s.dtype, features, fb, sim, block_idx, block_cnt, a,
+                                         static_cast<hipStream_t>(stream)));
 }
 
 const char* saf3r_status_string(int32_t status) {

@@ -17,8 +17,12 @@ enum Pattern : int32_t {
   kTopK = 2,
   kAnchor = 3,
   kStride = 4,
-  kGlobalProbe = 5
+  kGlobalProbe = 5,
+  kCosineTopK = 6
 };
+
+constexpr int kMaxCosineDim = 4096;   // feature width accepted by the cosine selection
+constexpr int kMaxCosinePerFrame = 64;  // key blocks kept per frame by a cosine head
 
 // ---------------------------------------------------------------- launches
 
@@ -73,6 +77,18 @@ struct AttnArgs {
   int32_t stride[kMaxHeads];  // by head index: key stride of a STRIDE head
 };
 
+// Block-wise DINO Top-K on caller-supplied per-token features.
+struct CosineArgs {
+  int64_t n;
+  int32_t nb;
+  int32_t cap;
+  int32_t dim;  // feature width
+  int32_t tokens_per_frame;
+  int32_t n_heads;
+  int16_t head[kMaxHeads];
+  int32_t topk[kMaxHeads];  // key blocks kept per frame
+};
+
 hipError_t launch_pool(int dtype, const void* q, const void* k, double* qp, double* kp,
                        const PoolArgs& a, hipStream_t s);
 hipError_t launch_select_topk(const double* qp, const double* kpT, int32_t* idx, int32_t* cnt,
@@ -80,6 +96,8 @@ hipError_t launch_select_topk(const double* qp, const double* kpT, int32_t* idx,
 hipError_t launch_select_static(int32_t* idx, int32_t* cnt, const StaticArgs& a, hipStream_t s);
 hipError_t launch_select_global(const double* qp, const double* kpT, int32_t* idx, int32_t* cnt,
                                 double* scores, const GlobalArgs& a, hipStream_t s);
+hipError_t launch_cosine(int dtype, const void* f, double* fb, double* sim, int32_t* idx,
+                         int32_t* cnt, const CosineArgs& a, hipStream_t s);
 hipError_t launch_attention(int dtype, const void* q, const void* k, const void* v,
                             const int32_t* idx, const int32_t* cnt, void* out, float* lse,
                             const AttnArgs& a, hipStream_t s);

@@ -70,7 +70,7 @@ def test_table_validation_and_capacity(B):
     assert cap(ctypes.byref(p), B.head_table([(0, 0)] * 3)) == 1
     assert cap(ctypes.byref(p), B.head_table([(0, 0), (2, 0), (2, 1)])) == -5
     assert cap(ctypes.byref(p), B.head_table([(0, 0), (2, 173), (2, 1)])) == -5
-    assert cap(ctypes.byref(p), B.head_table([(0, 0), (6, 1), (2, 1)])) == -5  # unknown class
+    assert cap(ctypes.byref(p), B.head_table([(0, 0), (7, 1), (2, 1)])) == -5  # unknown class
     assert cap(ctypes.byref(p), B.head_table([(0, 0), (-1, 1), (2, 1)])) == -5
     assert cap(ctypes.byref(p), None) == -1
     # frames of 128 tokens align with blocks: two blocks per frame
@@ -131,3 +131,29 @@ def test_status_strings(B):
     for s in (0, -1, -2, -3, -4, -5, 42):
         assert lib.saf3r_status_string(s)
     assert lib.saf3r_status_string(-3).decode().startswith("index capacity")
+
+
+def test_cosine_entry_points_validate_before_launch(B):
+    lib = B.load()
+    p = _p(B, heads=2, frames=8, T=1374)  # nb = 172
+    # workspace: (feat_dim * nb + nb^2) doubles
+    assert lib.saf3r_cosine_workspace_bytes(ctypes.byref(p), 64) == (64 * 172 + 172 * 172) * 8
+    assert lib.saf3r_cosine_workspace_bytes(ctypes.byref(p), 0) == -1
+    assert lib.saf3r_cosine_workspace_bytes(ctypes.byref(p), 4097) == -1
+    assert lib.saf3r_cosine_workspace_bytes(None, 64) == -1
+    cap = lib.saf3r_index_capacity
+    # frames of 1374 tokens: a key block counts under the frame of its first
+    # token, so frames hold 22 or 21 blocks (8 frames, 172 blocks)
+    assert cap(ctypes.byref(p), B.head_table([(B.COSINE_TOPK, 1), (0, 0)])) == 8
+    assert cap(ctypes.byref(p), B.head_table([(B.COSINE_TOPK, 2), (0, 0)])) == 16
+    assert cap(ctypes.byref(p), B.head_table([(B.COSINE_TOPK, 64), (0, 0)])) == 172
+    assert cap(ctypes.byref(p), B.head_table([(B.COSINE_TOPK, 65), (0, 0)])) == -5
+    assert cap(ctypes.byref(p), B.head_table([(B.COSINE_TOPK, 0), (0, 0)])) == -5
+    fake = ctypes.c_void_p(0x1000)  # never dereferenced: validation fails first
+    t = B.head_table([(B.COSINE_TOPK, 2), (0, 0)])
+    need = lib.saf3r_cosine_workspace_bytes(ctypes.byref(p), 64)
+    sel = lib.saf3r_cosine_select
+    assert sel(ctypes.byref(p), t, None, 64, fake, need, fake, fake, 16, None) == -1
+    assert sel(ctypes.byref(p), t, fake, 0, fake, need, fake, fake, 16, None) == -1
+    assert sel(ctypes.byref(p), t, fake, 64, fake, need - 8, fake, fake, 16, None) == -3
+    assert sel(ctypes.byref(p), t, fake, 64, fake, need, fake, fake, 15, None) == -3

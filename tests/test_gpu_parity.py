@@ -271,3 +271,57 @@ def test_stride_sampled_parity_large(gpu_lib, stride):
             o_ref, l_ref = O.attend_tokens(qh, kh, vh, r, keys)
             assert PT.max_abs(out[h][r.start:r.stop], o_ref) <= PT.TOL_BF16, (h, i)
             assert PT.max_abs(lse[h][r.start:r.stop], l_ref) <= PT.LSE_TOL_BF16, (h, i)
+
+
+# ------------------------------------------------------- cosine top-k
+
+
+def _features(n, dim, frames, T, seed):
+    """Synthetic per-token features: a per-frame shared direction plus noise,
+    so similar frames share structure (stand-in for DINO patch features)."""
+    g = np.random.default_rng(seed)
+    base = g.standard_normal((frames, dim))
+    f = np.repeat(base, T, axis=0)[:n] * 0.8 + g.standard_normal((n, dim))
+    return f.astype(np.float32)
+
+
+@pytest.mark.parametrize("frames,T,dtype,dim", [(8, 1374, "bf16", 64), (4, 261, "f32", 96),
+                                                (3, 100, "bf16", 33), (1, 129, "f32", 8)])
+def test_cosine_topk_lists_and_attention(gpu_lib, frames, T, dtype, dim):
+    import torch
+
+    import paper_2607_03612_amd as P
+
+    w = Workload(f"cos-{frames}x{T}-{dtype}", frames, T, dtype, ("fixed", 1, 1, 50), heads=4)
+    q, k, v = make_qkv(w)
+    f32 = _features(w.tokens, dim, frames, T, seed=frames + T)
+    if dtype == "bf16":  # round to bf16 bits (nearest even), as the inputs are
+        bits = f32.view(np.uint32)
+        f_in = ((bits + 0x7FFF + ((bits >> 16) & 1)) >> 16).astype(np.uint16)
+    else:
+        f_in = f32
+    f64 = O.to_f64(f_in, dtype)
+    table = [(O.COSINE_TOPK, 1), (O.COSINE_TOPK, 3), (O.TOPK, max(1, w.nb // 4)), (O.DENSE, 0)]
+    tq, tk, tv = (PT.to_device(x, dtype) for x in (q, k, v))
+    code = P.BF16 if dtype == "bf16" else P.F32
+    cap = P.index_capacity(table, frames, T, code)
+    idx = torch.full((4, w.nb, cap), -7, dtype=torch.int32, device="cuda")
+    cnt = torch.zeros((4, w.nb), dtype=torch.int32, device="cuda")
+    P.cosine_select(PT.to_device(f_in, dtype), table, frames, T, idx, cnt)
+    # select_blocks afterwards leaves the cosine rows as they are (cached lists)
+    qp, kp = P.estimate_blocks(tq, tk, table, frames, T)
+    P.select_blocks(qp, kp, table, frames, T, cap, idx, cnt, dtype=code)
+    out, lse = P.sparse_attention(tq, tk, tv, table, frames, T, idx, cnt, want_lse=True)
+    torch.cuda.synchronize()
+    res = {"idx": idx.cpu().numpy(), "cnt": cnt.cpu().numpy(), "out": PT.out_to_numpy(out),
+           "lse": lse.cpu().numpy().astype(np.float64)}
+    ref = O.run_layer(q, k, v, table, T, dtype, features=f64)
+    tol, lse_tol = _tols(w)
+    near = 0
+    for h, (pattern, _) in enumerate(table):
+        for i in range(w.nb):
+            status = PT.check_lists(res, h, i, pattern, ref["lists"][h][i], ref["margins"][h][i], w.nb, cap)
+            near += status == "near_tie"
+        assert PT.max_abs(res["out"][h], ref["out"][h]) <= tol, h
+        assert PT.max_abs(res["lse"][h], ref["lse"][h]) <= lse_tol, h
+    print(f"[parity] cosine {w.name}: near-ties {near}", flush=True)

@@ -335,3 +335,61 @@ def test_stride_attention_matches_library_with_token_mask(n, stride):
     if stride == 1:
         dense_out, _ = O.dense_attention(q, k, v)
         np.testing.assert_allclose(out, dense_out, rtol=1e-12, atol=1e-12)
+
+
+# ------------------------------------------------------ cosine top-k
+
+
+def _bruteforce_tile_cosine(f, block):
+    n = len(f)
+    nb = (n + block - 1) // block
+    norm = [math.sqrt(sum(x * x for x in row)) for row in f]
+    out = [[0.0] * nb for _ in range(nb)]
+    for i in range(nb):
+        for j in range(nb):
+            ti = range(i * block, min(n, (i + 1) * block))
+            tj = range(j * block, min(n, (j + 1) * block))
+            acc = 0.0
+            for t in ti:
+                for u in tj:
+                    acc += sum(f[t][e] * f[u][e] for e in range(len(f[0]))) / (norm[t] * norm[u])
+            out[i][j] = acc / (len(ti) * len(tj))
+    return np.array(out)
+
+
+@pytest.mark.parametrize("n,block,d", [(23, 4, 6), (16, 8, 3), (10, 10, 5)])
+def test_cosine_block_similarity_is_tile_mean_of_token_cosines(n, block, d):
+    f = _rand((n, d), 41) + 0.3
+    fb = O.cosine_block_features(f, block)
+    np.testing.assert_allclose(fb @ fb.T, _bruteforce_tile_cosine(f.tolist(), block), rtol=1e-12, atol=1e-12)
+    # unit tokens: a one-token block's feature has length 1
+    one = O.cosine_block_features(f, 1)
+    np.testing.assert_allclose(np.sum(one * one, axis=1), 1.0, rtol=1e-14)
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_cosine_topk_row_is_per_frame_bruteforce(seed):
+    g = np.random.default_rng(50 + seed)
+    T, block = 20, 4          # frames of 20 tokens, blocks of 4: block j is in frame (4j)//20
+    nb = 15                   # N = 60 tokens, 3 frames of 5 blocks each
+    sim = g.standard_normal(nb)
+    if seed % 2:
+        sim[[1, 3, 7]] = sim[0]  # planted ties
+    for k in (1, 2, 5, 6):
+        got, _ = O.cosine_topk_row(sim, k, T, block)
+        want = []
+        for f in range(3):
+            js = [j for j in range(nb) if (block * j) // T == f]
+            kk = min(k, len(js))
+            want += [js[x] for x in _bruteforce_topk([sim[j] for j in js], kk)]
+        assert list(got) == sorted(want)
+
+
+def test_cosine_topk_frame_of_a_straddling_block():
+    # T = 6, block = 4: block 1 holds tokens 4..7 (frames 0 and 1) and counts
+    # under frame 0, the frame of its first token
+    assert [O.block_frame(j, 6, 4) for j in range(5)] == [0, 0, 1, 2, 2]
+    sim = np.array([0.1, 0.9, 0.5, 0.2, 0.3])
+    got, margin = O.cosine_topk_row(sim, 1, 6, 4)
+    assert list(got) == [1, 2, 4]
+    assert margin == pytest.approx(min(0.9 - 0.1, 0.3 - 0.2))
