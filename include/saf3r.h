@@ -209,6 +209,16 @@ saf3r_status saf3r_cosine_select(const saf3r_problem* problem, const saf3r_head_
                                  int64_t workspace_bytes, int32_t* block_idx, int32_t* block_cnt,
                                  int32_t cap, void* stream);
 
+/* Approximation cost of Eq. 1 (Sec. 4.2, offline head profiling) for one
+ * input: per head h,
+ *   nmse_out[h] = sum (o_full - o_sparse)^2 / sum o_full^2
+ * over the head's N x 64 outputs, accumulated in float64 in a fixed order.
+ *   o_full, o_sparse  device [heads, N, 64] of problem->dtype (16-byte aligned)
+ *   nmse_out          device float64 [heads]
+ * Returns SAF3R_OK, or an error with nothing enqueued. */
+saf3r_status saf3r_nmse(const saf3r_problem* problem, const void* o_full, const void* o_sparse,
+                        double* nmse_out, void* stream);
+
 /* Static description of a status code (never NULL). */
 const char* saf3r_status_string(int32_t status);
 

@@ -16,6 +16,8 @@ from .saf3r_oracle import (  # noqa: F401
     attend_block,
     attend_head,
     attend_stride,
+    attention_flops,
+    baseline_stride,
     attend_tokens,
     block_range,
     block_frame,
@@ -29,6 +31,7 @@ from .saf3r_oracle import (  # noqa: F401
     nmse,
     num_blocks,
     pool_blocks,
+    progressive_substitution,
     run_layer,
     select_head,
     stride_keys,

@@ -29,8 +29,9 @@ fusion or reordering beyond what the definitions state:
    blocks whose features are most similar to the query block's.
 4. Attention restricted to the kept keys (Sec. 4.1, Query-Probe Top-K kernel):
    softmax over the kept key tokens, renormalised over that set, times V.
-5. NMSE (Sec. 4.2, Eq. 1) between full and sparse outputs, as a quality
-   report.
+5. NMSE (Sec. 4.2, Eq. 1) between full and sparse outputs, the attention
+   cost Omega in floating-point operations, and the progressive-substitution
+   choice of Eq. 2 (the offline head profiling).
 
 Pins (checked by the CPU tests, not by this module): pooling+scores against
 the brute-force tile mean of S; Top-K against brute force over all k-subsets;
@@ -332,6 +333,41 @@ def nmse(o_full: np.ndarray, o_sparse: np.ndarray) -> float:
     num = float(np.sum((o_full - o_sparse) ** 2))
     den = float(np.sum(o_full ** 2))
     return num / den
+
+
+def attention_flops(n: int, d: int, block: int, lists=None, stride: int = 0) -> int:
+    """Omega(c) of Eq. 2: floating-point operations of attention restricted
+    to the kept keys, 4 d per (query token, kept key token) pair (the Q K^T
+    and P V products). Pass the per-query-block lists, or ``stride`` for the
+    uniform sampling kernel."""
+    if stride:
+        return 4 * d * n * len(stride_keys(n, stride))
+    total = 0
+    for i, kept in enumerate(lists):
+        keys = sum(len(block_range(int(j), n, block)) for j in kept)
+        total += 4 * d * len(block_range(i, n, block)) * keys
+    return total
+
+
+def progressive_substitution(errors, costs) -> int:
+    """Eq. 2 by progressive substitution (Sec. 4.2): entry 0 is the baseline
+    c_base; walking the candidates in order, the current choice is replaced
+    whenever a candidate has a strictly lower error and a cost not above the
+    baseline's. Returns the index of c*."""
+    best = 0
+    for c in range(1, len(errors)):
+        if costs[c] <= costs[0] and errors[c] < errors[best]:
+            best = c
+    return best
+
+
+def baseline_stride(sigma: float) -> int:
+    """Stride of the uniform sampling baseline with sparsity at least sigma:
+    the smallest s with 1 - 1/s >= sigma."""
+    s = 1
+    while 1.0 - 1.0 / s < sigma - 1e-12:
+        s += 1
+    return s
 
 
 # --------------------------------------------------------------------------

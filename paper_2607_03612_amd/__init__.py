@@ -19,6 +19,7 @@ from .binding import (  # noqa: F401
     estimate_blocks,
     index_capacity,
     load,
+    nmse,
     num_blocks,
     run_layer,
     select_blocks,

@@ -11,7 +11,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libsaf3r.so")
-SOURCES = ["api.cpp", "pool.hip", "select.hip", "attn.hip", "cosine.hip"]
+SOURCES = ["api.cpp", "pool.hip", "select.hip", "attn.hip", "cosine.hip", "nmse.hip"]
 ARCH = "gfx950"
 
 

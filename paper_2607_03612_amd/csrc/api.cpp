@@ -336,6 +336,16 @@ saf3r_status saf3r_cosine_select(const saf3r_problem* problem, const saf3r_head_
                                          static_cast<hipStream_t>(stream)));
 }
 
+saf3r_status saf3r_nmse(const saf3r_problem* problem, const void* o_full, const void* o_sparse,
+                        double* nmse_out, void* stream) {
+  Shape s;
+  const saf3r_status st = check_problem(problem, &s);
+  if (st != SAF3R_OK) return st;
+  if (!o_full || !o_sparse || !nmse_out) return SAF3R_ERR_INVALID_ARGUMENT;
+  return hip_status(saf3r::launch_nmse(s.dtype, o_full, o_sparse, nmse_out, s.heads, s.n,
+                                       static_cast<hipStream_t>(stream)));
+}
+
 const char* saf3r_status_string(int32_t status) {
   switch (status) {
     case SAF3R_OK: return "ok";

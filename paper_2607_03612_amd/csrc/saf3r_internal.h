@@ -98,6 +98,8 @@ hipError_t launch_select_global(const double* qp, const double* kpT, int32_t* id
                                 double* scores, const GlobalArgs& a, hipStream_t s);
 hipError_t launch_cosine(int dtype, const void* f, double* fb, double* sim, int32_t* idx,
                          int32_t* cnt, const CosineArgs& a, hipStream_t s);
+hipError_t launch_nmse(int dtype, const void* ref, const void* test, double* out, int heads,
+                       int64_t n, hipStream_t s);
 hipError_t launch_attention(int dtype, const void* q, const void* k, const void* v,
                             const int32_t* idx, const int32_t* cnt, void* out, float* lse,
                             const AttnArgs& a, hipStream_t s);

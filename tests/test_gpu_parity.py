@@ -325,3 +325,62 @@ def test_cosine_topk_lists_and_attention(gpu_lib, frames, T, dtype, dim):
         assert PT.max_abs(res["out"][h], ref["out"][h]) <= tol, h
         assert PT.max_abs(res["lse"][h], ref["lse"][h]) <= lse_tol, h
     print(f"[parity] cosine {w.name}: near-ties {near}", flush=True)
+
+
+# ------------------------------------------------- NMSE and the profiler
+
+
+def test_nmse_kernel_matches_oracle(gpu_lib):
+    import paper_2607_03612_amd as P
+
+    for dtype in ("bf16", "f32"):
+        w = Workload(f"nmse-{dtype}", 3, 261, dtype, ("fixed", 1, 1, 50), heads=3)
+        a, b, _ = make_qkv(w, seed=3)
+        ta, tb = PT.to_device(a, dtype), PT.to_device(b, dtype)
+        got = P.nmse(ta, tb, w.frames, w.tokens_per_frame).cpu().numpy()
+        for h in range(3):
+            want = O.nmse(O.to_f64(a[h], dtype), O.to_f64(b[h], dtype))
+            assert abs(got[h] - want) <= 1e-12 * want, (dtype, h, got[h], want)
+        assert np.all(P.nmse(ta, ta, w.frames, w.tokens_per_frame).cpu().numpy() == 0.0)
+
+
+def test_profiler_matches_oracle_search(gpu_lib):
+    """Errors and costs of every (configuration, head) against the oracle's
+    NMSE of Eq. 1 and FLOP count, and the Eq. 2 choice where the errors of
+    the two best eligible configurations are clearly apart."""
+    import paper_2607_03612_amd as P
+    from paper_2607_03612_amd import profiler
+
+    w = Workload("profile", 4, 261, "bf16", ("fixed", 0, 0, 50), heads=4)
+    calib = [make_qkv(w, seed=s) for s in (11, 12)]
+    dev = [tuple(PT.to_device(x, "bf16") for x in qkv) for qkv in calib]
+    nb = w.nb
+    cands = [(O.TOPK, 1), (O.TOPK, 2), (O.TOPK, 3), (O.GLOBAL_PROBE, 2), (O.FRAME_LOCAL, 0),
+             (O.ANCHOR, 0), (O.STRIDE, 10)]
+    res = profiler.profile_heads(dev, w.frames, w.tokens_per_frame, cands, sigma=0.85)
+    configs = res["configs"]
+    assert configs[0] == (O.STRIDE, O.baseline_stride(0.85))
+    H, n = w.heads, w.tokens
+    err_ref = np.zeros((len(configs), H))
+    cost_ref = np.zeros((len(configs), H))
+    for q, k, v in calib:
+        for c, (pattern, param) in enumerate(configs):
+            ref = O.run_layer(q, k, v, [(pattern, param)] * H, w.tokens_per_frame, "bf16")
+            for h in range(H):
+                qh, kh, vh = (O.to_f64(x[h], "bf16") for x in (q, k, v))
+                full, _ = O.dense_attention(qh, kh, vh)
+                err_ref[c, h] += O.nmse(full, ref["out"][h]) / len(calib)
+                if pattern == O.STRIDE:
+                    cost_ref[c, h] += O.attention_flops(n, 64, 64, stride=param) / len(calib)
+                else:
+                    cost_ref[c, h] += O.attention_flops(n, 64, 64, ref["lists"][h]) / len(calib)
+    # exact counts; a near-tie row may keep a different block (rtol covers it)
+    np.testing.assert_allclose(res["costs"], cost_ref, rtol=1e-3, atol=0)
+    # bf16 outputs on both sides of the GPU error: a few 1e-3 relative
+    np.testing.assert_allclose(res["errors"], err_ref, rtol=3e-2, atol=1e-5)
+    for h in range(H):
+        want = O.progressive_substitution(err_ref[:, h], cost_ref[:, h])
+        eligible = sorted(err_ref[c, h] for c in range(len(configs)) if cost_ref[c, h] <= cost_ref[0, h])
+        if len(eligible) < 2 or eligible[1] - eligible[0] > 0.1 * eligible[0]:
+            assert res["choice"][h] == want, (h, res["errors"][:, h], err_ref[:, h])
+    print(f"[profile] choice {res['choice']} table {res['table']}", flush=True)

@@ -393,3 +393,45 @@ def test_cosine_topk_frame_of_a_straddling_block():
     got, margin = O.cosine_topk_row(sim, 1, 6, 4)
     assert list(got) == [1, 2, 4]
     assert margin == pytest.approx(min(0.9 - 0.1, 0.3 - 0.2))
+
+
+# ------------------------------------------------ offline profiling (Eq. 1-2)
+
+
+def test_attention_flops_counts_token_pairs():
+    # lists: query block 0 (64 tokens) keeps blocks {0, 2}; block 1 keeps {1};
+    # block 2 (partial: 20 tokens) keeps {0, 1, 2}; d = 8 -> 4 d = 32 per pair
+    n, d, block = 148, 8, 64
+    lists = [np.array([0, 2]), np.array([1]), np.array([0, 1, 2])]
+    pairs = 64 * (64 + 20) + 64 * 64 + 20 * (64 + 64 + 20)
+    assert O.attention_flops(n, d, block, lists) == 32 * pairs
+    # stride: every query against ceil(n / s) keys
+    assert O.attention_flops(10, d, block, stride=3) == 32 * 10 * 4
+    # dense lists equal 4 d n^2
+    dense = [np.arange(3)] * 3
+    assert O.attention_flops(n, d, block, dense) == 4 * d * n * n
+
+
+def test_progressive_substitution_follows_eq2():
+    # base error 0.5 cost 10; candidate 2 is best but too costly; candidate 3
+    # ties candidate 1 and comes later (no replacement on ties)
+    errors = [0.5, 0.2, 0.05, 0.2, 0.3]
+    costs = [10, 10, 11, 9, 8]
+    assert O.progressive_substitution(errors, costs) == 1
+    assert O.progressive_substitution([0.1, 0.2, 0.3], [5, 5, 5]) == 0  # base stays
+    assert O.progressive_substitution([0.1, 0.0], [5, 6]) == 0          # over budget
+    assert O.progressive_substitution([0.1, 0.0], [5, 5]) == 1
+    # equals the constrained argmin with ties to the earlier entry
+    g = np.random.default_rng(61)
+    for _ in range(50):
+        e = g.integers(0, 4, 8).astype(float)
+        c = g.integers(0, 5, 8)
+        ok = [i for i in range(8) if c[i] <= c[0]]
+        assert O.progressive_substitution(e, c) == min(ok, key=lambda i: (e[i], i))
+
+
+def test_baseline_stride_reaches_the_sparsity():
+    assert O.baseline_stride(0.85) == 7   # keeps 1/7 = 14.3% of keys
+    assert O.baseline_stride(0.5) == 2
+    assert O.baseline_stride(0.0) == 1
+    assert O.baseline_stride(0.75) == 4
