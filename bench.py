@@ -116,6 +116,59 @@ def blas_threads():
         return os.cpu_count() or 1
 
 
+def event_ms(torch, fn, reps):
+    """Mean milliseconds of ``fn`` over ``reps`` launches (one untimed first)."""
+    fn()
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(reps):
+        fn()
+    b.record()
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) / reps
+
+
+def measure_next_rows(P, torch, w, tq, tk, tv, out, table):
+    H, N, nb, S, T = w.heads, w.tokens, w.nb, w.frames, w.tokens_per_frame
+    dev = tq.device
+    res = {}
+    # uniform stride 7 on every head: 137400 queries x 19629 keys per head
+    stride = 7
+    st_tab = [(P.STRIDE, stride)] * H
+    ms = event_ms(torch, lambda: P.sparse_attention(tq, tk, tv, st_tab, S, T, out=out), 2)
+    flop = 4 * 64 * N * (-(-N // stride)) * H
+    res["stride_attention"] = {"stride": stride, "ms": round(ms, 3),
+                               "tflops": round(flop / (ms * 1e-3) / 1e12, 1)}
+    # paper-literal global probe on the Top-K heads of the table
+    g_tab = [(P.GLOBAL_PROBE, p) if c == P.TOPK else (c, p) for c, p in table]
+    cap = P.index_capacity(g_tab, S, T)
+    qp, kp = P.estimate_blocks(tq, tk, g_tab, S, T)
+    idx = torch.empty((H, nb, cap), dtype=torch.int32, device=dev)
+    cnt = torch.empty((H, nb), dtype=torch.int32, device=dev)
+    ms = event_ms(torch, lambda: P.select_blocks(qp, kp, g_tab, S, T, cap, idx, cnt), 5)
+    res["global_probe_select"] = {"heads": sum(c == P.GLOBAL_PROBE for c, _ in g_tab), "ms": round(ms, 4)}
+    # per-frame cosine Top-K (2 key blocks per frame) on 1024-wide bf16 features
+    dim = 1024
+    feats = (torch.randn((N, dim), device=dev, generator=torch.Generator(device=dev).manual_seed(0))
+             .to(torch.bfloat16))
+    c_tab = [(P.COSINE_TOPK, 2)] * H
+    ccap = P.index_capacity(c_tab, S, T)
+    cidx = torch.empty((H, nb, ccap), dtype=torch.int32, device=dev)
+    ccnt = torch.empty((H, nb), dtype=torch.int32, device=dev)
+    ws = torch.empty(P.cosine_workspace_bytes(S, T, dim, H) // 8, dtype=torch.float64, device=dev)
+    ms = event_ms(torch, lambda: P.cosine_select(feats, c_tab, S, T, cidx, ccnt, workspace=ws), 2)
+    res["cosine_select"] = {"feat_dim": dim, "per_frame": 2, "ms": round(ms, 3),
+                            "sim_fp64_tflops": round(2 * nb * nb * dim / (ms * 1e-3) / 1e12, 2)}
+    del ws, feats
+    # Eq. 1 error of two outputs of the layer
+    other = out.clone()
+    ms = event_ms(torch, lambda: P.nmse(out, other, S, T), 3)
+    nbytes = 2 * out.numel() * out.element_size()
+    res["nmse"] = {"ms": round(ms, 3), "gbps": round(nbytes / (ms * 1e-3) / 1e9, 1)}
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -126,6 +179,8 @@ def main():
     ap.add_argument("--dense-reps", type=int, default=3)
     ap.add_argument("--cpu-rows", type=int, default=320,
                     help="query blocks per head in the oracle CPU sample (0 = skip)")
+    ap.add_argument("--next-rows", type=int, default=1,
+                    help="also time the stride, global-probe, cosine and NMSE kernels (0 = skip)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run three device-to-device copies of MIB MiB (a plain copy "
                          "kernel of known size, to scale rocprofv3 FETCH_SIZE / WRITE_SIZE) and exit")
@@ -271,6 +326,15 @@ def main():
     ref_cold_ms = cold_ms(lambda: sink.copy_(ref_buf.sum()))
     del flush_buf, ref_buf
 
+    # the other pattern classes and the profiler's error kernel on the same
+    # layer: uniform stride (the profiling baseline at sparsity 0.85),
+    # global-probe selection, per-frame cosine selection on 1024-wide
+    # features, and the Eq. 1 error
+    next_rows = None
+    if args.next_rows:
+        next_rows = measure_next_rows(P, torch, w, tq, tk, tv, out, table)
+        log(f"[bench] next rows {next_rows}")
+
     cpu = None
     if args.cpu_rows > 0:
         t0 = time.perf_counter()
@@ -321,6 +385,7 @@ def main():
             "stream_read_reference_GBps": round(est_bytes / (ref_cold_ms * 1e-3) / 1e9, 1),
         },
         "dense_baseline": dense,
+        "next_rows": next_rows,
         "cpu_baseline": cpu,
     }
     print(json.dumps(result), flush=True)
