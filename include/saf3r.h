@@ -75,7 +75,13 @@ typedef enum { SAF3R_F32 = 0, SAF3R_BF16 = 1 } saf3r_dtype;
  *                       frame, the param key blocks whose caller-supplied
  *                       features are most similar to the query block's;
  *                       param in [1, 64]. Lists come from
- *                       saf3r_cosine_select, once per sequence.
+ *                       saf3r_cosine_select, once per sequence;
+ *   SAF3R_SKIP          not a pattern: every call leaves the head's pooled
+ *                       data, lists, counts, outputs and lse untouched. A
+ *                       caller splits one layer into independent launches
+ *                       (e.g. static heads on one stream while the Top-K
+ *                       heads are pooled and selected on another) by
+ *                       marking the other heads SKIP; param unused.
  */
 typedef enum {
   SAF3R_DENSE = 0,
@@ -84,7 +90,8 @@ typedef enum {
   SAF3R_ANCHOR = 3,
   SAF3R_STRIDE = 4,
   SAF3R_GLOBAL_PROBE = 5,
-  SAF3R_COSINE_TOPK = 6
+  SAF3R_COSINE_TOPK = 6,
+  SAF3R_SKIP = 7
 } saf3r_pattern;
 
 typedef struct {

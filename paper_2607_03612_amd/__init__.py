@@ -23,6 +23,7 @@ from .binding import (  # noqa: F401
     num_blocks,
     run_layer,
     select_blocks,
+    SKIP,
     sparse_attention,
     STRIDE,
 )

@@ -13,7 +13,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG, "libsaf3r.so")
 
 F32, BF16 = 0, 1
-DENSE, FRAME_LOCAL, TOPK, ANCHOR, STRIDE, GLOBAL_PROBE, COSINE_TOPK = 0, 1, 2, 3, 4, 5, 6
+DENSE, FRAME_LOCAL, TOPK, ANCHOR, STRIDE, GLOBAL_PROBE, COSINE_TOPK, SKIP = 0, 1, 2, 3, 4, 5, 6, 7
 HEAD_DIM = 64
 BLOCK = 64
 

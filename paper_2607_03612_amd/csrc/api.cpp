@@ -52,6 +52,7 @@ saf3r_status check_table(const Shape& s, const saf3r_head_cfg* t) {
     switch (t[h].pattern) {
       case SAF3R_DENSE:
       case SAF3R_FRAME_LOCAL:
+      case SAF3R_SKIP:
         break;
       case SAF3R_TOPK:
       case SAF3R_GLOBAL_PROBE:
@@ -197,8 +198,8 @@ saf3r_status saf3r_select_blocks(const saf3r_problem* problem, const saf3r_head_
     } else if (table[h].pattern == SAF3R_GLOBAL_PROBE) {
       ga.head[ga.n_heads] = (int16_t)h;
       ga.topk[ga.n_heads++] = table[h].param;
-    } else if (table[h].pattern == SAF3R_COSINE_TOPK) {
-      // lists come from saf3r_cosine_select and are left as they are
+    } else if (table[h].pattern == SAF3R_COSINE_TOPK || table[h].pattern == SAF3R_SKIP) {
+      // cosine lists come from saf3r_cosine_select; skipped heads stay as they are
     } else {
       sa.head[sa.n_heads] = (int16_t)h;
       sa.pattern[sa.n_heads] = (int8_t)table[h].pattern;
@@ -237,7 +238,7 @@ saf3r_status saf3r_sparse_attention(const saf3r_problem* problem, const saf3r_he
   bool needs_lists = false;
   for (int h = 0; h < s.heads; ++h) {
     const int p = table[h].pattern;
-    needs_lists = needs_lists || (p != SAF3R_DENSE && p != SAF3R_STRIDE);
+    needs_lists = needs_lists || (p != SAF3R_DENSE && p != SAF3R_STRIDE && p != SAF3R_SKIP);
   }
   if (needs_lists) {
     if (!block_idx || !block_cnt) return SAF3R_ERR_INVALID_ARGUMENT;
@@ -260,6 +261,7 @@ saf3r_status saf3r_sparse_attention(const saf3r_problem* problem, const saf3r_he
   bool all_dense = true;
   for (int h = 0; h < s.heads; ++h) {
     const int p = table[h].pattern;
+    if (p == SAF3R_SKIP) continue;
     a.dense[h] = p == SAF3R_DENSE ? 1 : 0;
     sa.stride[h] = p == SAF3R_STRIDE ? table[h].param : 1;
     switch (p) {

@@ -70,7 +70,7 @@ def test_table_validation_and_capacity(B):
     assert cap(ctypes.byref(p), B.head_table([(0, 0)] * 3)) == 1
     assert cap(ctypes.byref(p), B.head_table([(0, 0), (2, 0), (2, 1)])) == -5
     assert cap(ctypes.byref(p), B.head_table([(0, 0), (2, 173), (2, 1)])) == -5
-    assert cap(ctypes.byref(p), B.head_table([(0, 0), (7, 1), (2, 1)])) == -5  # unknown class
+    assert cap(ctypes.byref(p), B.head_table([(0, 0), (8, 1), (2, 1)])) == -5  # unknown class
     assert cap(ctypes.byref(p), B.head_table([(0, 0), (-1, 1), (2, 1)])) == -5
     assert cap(ctypes.byref(p), None) == -1
     # frames of 128 tokens align with blocks: two blocks per frame
@@ -157,3 +157,16 @@ def test_cosine_entry_points_validate_before_launch(B):
     assert sel(ctypes.byref(p), t, fake, 0, fake, need, fake, fake, 16, None) == -1
     assert sel(ctypes.byref(p), t, fake, 64, fake, need - 8, fake, fake, 16, None) == -3
     assert sel(ctypes.byref(p), t, fake, 64, fake, need, fake, fake, 15, None) == -3
+
+
+def test_skip_heads_are_accepted_and_need_nothing(B):
+    lib = B.load()
+    cap = lib.saf3r_index_capacity
+    p = _p(B, heads=3, frames=8, T=1374)
+    assert cap(ctypes.byref(p), B.head_table([(B.SKIP, 0)] * 3)) == 1
+    assert cap(ctypes.byref(p), B.head_table([(B.SKIP, 99), (2, 13), (B.SKIP, -4)])) == 13
+    fake = ctypes.c_void_p(0x1000)
+    # a table of SKIP and DENSE heads needs no lists: a missing output fails first
+    t = B.head_table([(B.SKIP, 0), (0, 0), (B.SKIP, 0)])
+    assert lib.saf3r_sparse_attention(ctypes.byref(p), t, fake, fake, fake, None, None, 0,
+                                      None, None, None) == -1

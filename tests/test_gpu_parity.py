@@ -384,3 +384,51 @@ def test_profiler_matches_oracle_search(gpu_lib):
         if len(eligible) < 2 or eligible[1] - eligible[0] > 0.1 * eligible[0]:
             assert res["choice"][h] == want, (h, res["errors"][:, h], err_ref[:, h])
     print(f"[profile] choice {res['choice']} table {res['table']}", flush=True)
+
+
+def test_skip_heads_split_a_layer_across_streams(gpu_lib):
+    """Static heads on one stream and Top-K heads on another (the rest marked
+    SKIP in each call) give the same lists and outputs as one call, and a
+    SKIP head's output is left untouched."""
+    import torch
+
+    import paper_2607_03612_amd as P
+
+    w = WORKLOADS["S8xT1374-bf16"]
+    q, k, v = make_qkv(w, seed=2)
+    table = make_table(w)
+    S, T, H, nb = w.frames, w.tokens_per_frame, w.heads, w.nb
+    tq, tk, tv = (PT.to_device(x, "bf16") for x in (q, k, v))
+    cap = P.index_capacity(table, S, T)
+    ref_out, ref_idx, ref_cnt = P.run_layer(tq, tk, tv, table, S, T)
+    dyn = [(p, a) if p == P.TOPK else (P.SKIP, 0) for p, a in table]
+    sta = [(P.SKIP, 0) if p == P.TOPK else (p, a) for p, a in table]
+    qp = torch.zeros((H, nb, 64), dtype=torch.float64, device="cuda")
+    kp = torch.zeros((H, 64, nb), dtype=torch.float64, device="cuda")
+    idx = torch.full((H, nb, cap), -9, dtype=torch.int32, device="cuda")
+    cnt = torch.full((H, nb), -9, dtype=torch.int32, device="cuda")
+    out = torch.full_like(tq, 7.0)
+    side = torch.cuda.Stream()
+    fork = torch.cuda.Event()
+    fork.record()
+    side.wait_event(fork)
+    with torch.cuda.stream(side):
+        P.select_blocks(qp, kp, sta, S, T, cap, idx, cnt)
+        P.sparse_attention(tq, tk, tv, sta, S, T, idx, cnt, out)
+    P.estimate_blocks(tq, tk, dyn, S, T, qp, kp)
+    P.select_blocks(qp, kp, dyn, S, T, cap, idx, cnt)
+    P.sparse_attention(tq, tk, tv, dyn, S, T, idx, cnt, out)
+    join = torch.cuda.Event()
+    join.record(side)
+    torch.cuda.current_stream().wait_event(join)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(out.cpu().float().numpy(), ref_out.cpu().float().numpy())
+    np.testing.assert_array_equal(cnt.cpu().numpy(), ref_cnt.cpu().numpy())
+    for h, (p, _) in enumerate(table):
+        if p != P.DENSE:
+            np.testing.assert_array_equal(idx[h].cpu().numpy(), ref_idx[h].cpu().numpy())
+    # an all-SKIP call touches nothing
+    before = out.clone()
+    P.sparse_attention(tq, tk, tv, [(P.SKIP, 0)] * H, S, T, idx, cnt, out)
+    torch.cuda.synchronize()
+    assert torch.equal(before, out)
