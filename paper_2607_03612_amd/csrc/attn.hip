@@ -475,12 +475,15 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
     mfma_pv(vA, p_new);
   }
 
-  // epilogue: normalise, round to bf16, store; log-sum-exp in natural log
+  // epilogue: normalise and round to bf16 into the (now idle) K half buffers
+  // (query rows 0..31 in one, 32..63 in the other, same swizzle), then store
+  // full 128-byte rows: eight 1 KB stores; log-sum-exp in natural log
 #pragma unroll
   for (int tq = 0; tq < 2; ++tq) {
     const float lt = pair_sum(l[tq]);
     const float inv = 1.0f / lt;
     const int query = w.i * kBlock + 32 * tq + l32;
+    lds_char* const ob = tq ? kbuf1 : kbuf0;
 #pragma unroll
     for (int c = 0; c < 2; ++c)
 #pragma unroll
@@ -488,12 +491,19 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
         bf16x4 ov;
 #pragma unroll
         for (int r = 0; r < 4; ++r) ov[r] = (__bf16)(o[c][tq][4 * g + r] * inv);
-        __builtin_amdgcn_raw_buffer_store_b64(
-            __builtin_bit_cast(i32x2, ov), ro,
-            (int)((query * kHeadDim + 32 * c + 8 * g + 4 * hf) * 2), 0, 0);
+        *(lds_bf16x4*)(ob + swz(l32, 4 * c + g) + 8 * hf) = ov;
       }
     if (lse && hf == 0 && query < a.n)
       lse[(int64_t)w.h * a.n + query] = (m[tq] + __log2f(lt)) * kLn2;
+  }
+#pragma unroll
+  for (int n = 0; n < 8; ++n) {
+    const int row = 8 * n + (lane >> 3);
+    const int chunk = lane & 7;
+    lds_char* const ob = row >= 32 ? kbuf1 : kbuf0;
+    const bf16x8 val = *(lds_bf16x8*)(ob + swz(row & 31, chunk));
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(i32x4, val), ro,
+                                           (int)(((w.i * kBlock + row) * kHeadDim + 8 * chunk) * 2), 0, 0);
   }
 }
 
