@@ -163,7 +163,9 @@ def measure_next_rows(P, torch, w, tq, tk, tv, out, table):
     del ws, feats
     # Eq. 1 error of two outputs of the layer
     other = out.clone()
-    ms = event_ms(torch, lambda: P.nmse(out, other, S, T), 3)
+    nws = torch.empty(P.nmse_workspace_bytes(w.heads, S, T) // 8, dtype=torch.float64, device=dev)
+    nout = torch.empty(w.heads, dtype=torch.float64, device=dev)
+    ms = event_ms(torch, lambda: P.nmse(out, other, S, T, out=nout, workspace=nws), 3)
     nbytes = 2 * out.numel() * out.element_size()
     res["nmse"] = {"ms": round(ms, 3), "gbps": round(nbytes / (ms * 1e-3) / 1e9, 1)}
     return res

@@ -42,7 +42,7 @@ typedef enum {
   SAF3R_OK = 0,
   SAF3R_ERR_INVALID_ARGUMENT = -1, /* null pointer, non-positive size, bad dtype */
   SAF3R_ERR_UNSUPPORTED = -2,      /* head_dim or block other than 64, sizes beyond the limits */
-  SAF3R_ERR_CAPACITY = -3,         /* cap smaller than saf3r_index_capacity() */
+  SAF3R_ERR_CAPACITY = -3,         /* cap or a workspace smaller than required */
   SAF3R_ERR_HIP = -4,              /* the HIP runtime reported an error on launch */
   SAF3R_ERR_BAD_TABLE = -5         /* unknown pattern class, or a class parameter out of range */
 } saf3r_status;
@@ -216,15 +216,25 @@ saf3r_status saf3r_cosine_select(const saf3r_problem* problem, const saf3r_head_
                                  int64_t workspace_bytes, int32_t* block_idx, int32_t* block_cnt,
                                  int32_t cap, void* stream);
 
+/* Device workspace of saf3r_nmse in bytes (heads x 128 float64 pairs), or
+ * a negative status for a bad problem. */
+int64_t saf3r_nmse_workspace_bytes(const saf3r_problem* problem);
+
 /* Approximation cost of Eq. 1 (Sec. 4.2, offline head profiling) for one
  * input: per head h,
  *   nmse_out[h] = sum (o_full - o_sparse)^2 / sum o_full^2
- * over the head's N x 64 outputs, accumulated in float64 in a fixed order.
+ * over the head's N x 64 outputs, accumulated in float64 in a fixed order
+ * (the same bits on every call with the same inputs).
  *   o_full, o_sparse  device [heads, N, 64] of problem->dtype (16-byte aligned)
+ *   workspace         device, >= saf3r_nmse_workspace_bytes bytes, 16-byte
+ *                     aligned; overwritten with per-slice partial sums
  *   nmse_out          device float64 [heads]
- * Returns SAF3R_OK, or an error with nothing enqueued. */
+ * Returns SAF3R_OK; SAF3R_ERR_INVALID_ARGUMENT for a null pointer;
+ * SAF3R_ERR_CAPACITY for a workspace that is too small; nothing is enqueued
+ * on an error. */
 saf3r_status saf3r_nmse(const saf3r_problem* problem, const void* o_full, const void* o_sparse,
-                        double* nmse_out, void* stream);
+                        void* workspace, int64_t workspace_bytes, double* nmse_out,
+                        void* stream);
 
 /* Static description of a status code (never NULL). */
 const char* saf3r_status_string(int32_t status);

@@ -20,6 +20,7 @@ from .binding import (  # noqa: F401
     index_capacity,
     load,
     nmse,
+    nmse_workspace_bytes,
     num_blocks,
     run_layer,
     select_blocks,

@@ -25,6 +25,7 @@ EXPORTS = (
     "saf3r_sparse_attention",
     "saf3r_cosine_workspace_bytes",
     "saf3r_cosine_select",
+    "saf3r_nmse_workspace_bytes",
     "saf3r_nmse",
     "saf3r_status_string",
 )
@@ -65,7 +66,9 @@ def _declare(lib):
     lib.saf3r_cosine_workspace_bytes.restype = ctypes.c_int64
     lib.saf3r_cosine_select.argtypes = [P, C, V, I32, V, ctypes.c_int64, V, V, I32, V]
     lib.saf3r_cosine_select.restype = I32
-    lib.saf3r_nmse.argtypes = [P, V, V, V, V]
+    lib.saf3r_nmse_workspace_bytes.argtypes = [P]
+    lib.saf3r_nmse_workspace_bytes.restype = ctypes.c_int64
+    lib.saf3r_nmse.argtypes = [P, V, V, V, ctypes.c_int64, V, V]
     lib.saf3r_nmse.restype = I32
     lib.saf3r_status_string.argtypes = [I32]
     lib.saf3r_status_string.restype = ctypes.c_char_p
@@ -254,17 +257,29 @@ def cosine_select(features, table, frames, tokens_per_frame, block_idx, block_cn
     return block_idx, block_cnt
 
 
-def nmse(o_full, o_sparse, frames, tokens_per_frame, out=None, stream=None):
+def nmse_workspace_bytes(heads, frames, tokens_per_frame, dtype=BF16) -> int:
+    p = problem(heads, frames, tokens_per_frame, dtype)
+    r = _lib().saf3r_nmse_workspace_bytes(ctypes.byref(p))
+    _check(min(r, 0), "saf3r_nmse_workspace_bytes")
+    return int(r)
+
+
+def nmse(o_full, o_sparse, frames, tokens_per_frame, out=None, workspace=None, stream=None):
     """Per-head ``||o_full - o_sparse||^2 / ||o_full||^2`` (float64 ``[H]``)."""
     import torch
 
     _check_qkv(o_full, o_sparse)
     H, N, _ = o_full.shape
+    dtype = _torch_dtype_code(o_full)
     if out is None:
         out = torch.empty(H, dtype=torch.float64, device=o_full.device)
-    p = problem(H, frames, tokens_per_frame, _torch_dtype_code(o_full))
-    _check(_lib().saf3r_nmse(ctypes.byref(p), _ptr(o_full), _ptr(o_sparse), _ptr(out),
-                             _stream(stream)), "saf3r_nmse")
+    need = nmse_workspace_bytes(H, frames, tokens_per_frame, dtype)
+    if workspace is None:
+        workspace = torch.empty(need // 8, dtype=torch.float64, device=o_full.device)
+    p = problem(H, frames, tokens_per_frame, dtype)
+    _check(_lib().saf3r_nmse(ctypes.byref(p), _ptr(o_full), _ptr(o_sparse), _ptr(workspace),
+                             ctypes.c_int64(workspace.numel() * workspace.element_size()),
+                             _ptr(out), _stream(stream)), "saf3r_nmse")
     return out
 
 

@@ -338,14 +338,23 @@ saf3r_status saf3r_cosine_select(const saf3r_problem* problem, const saf3r_head_
                                          static_cast<hipStream_t>(stream)));
 }
 
-saf3r_status saf3r_nmse(const saf3r_problem* problem, const void* o_full, const void* o_sparse,
-                        double* nmse_out, void* stream) {
+int64_t saf3r_nmse_workspace_bytes(const saf3r_problem* problem) {
   Shape s;
   const saf3r_status st = check_problem(problem, &s);
   if (st != SAF3R_OK) return st;
-  if (!o_full || !o_sparse || !nmse_out) return SAF3R_ERR_INVALID_ARGUMENT;
-  return hip_status(saf3r::launch_nmse(s.dtype, o_full, o_sparse, nmse_out, s.heads, s.n,
-                                       static_cast<hipStream_t>(stream)));
+  return (int64_t)s.heads * saf3r::kNmseParts * 2 * (int64_t)sizeof(double);
+}
+
+saf3r_status saf3r_nmse(const saf3r_problem* problem, const void* o_full, const void* o_sparse,
+                        void* workspace, int64_t workspace_bytes, double* nmse_out,
+                        void* stream) {
+  Shape s;
+  const saf3r_status st = check_problem(problem, &s);
+  if (st != SAF3R_OK) return st;
+  if (!o_full || !o_sparse || !workspace || !nmse_out) return SAF3R_ERR_INVALID_ARGUMENT;
+  if (workspace_bytes < saf3r_nmse_workspace_bytes(problem)) return SAF3R_ERR_CAPACITY;
+  return hip_status(saf3r::launch_nmse(s.dtype, o_full, o_sparse, workspace, nmse_out, s.heads,
+                                       s.n, static_cast<hipStream_t>(stream)));
 }
 
 const char* saf3r_status_string(int32_t status) {
@@ -353,7 +362,7 @@ const char* saf3r_status_string(int32_t status) {
     case SAF3R_OK: return "ok";
     case SAF3R_ERR_INVALID_ARGUMENT: return "invalid argument (null pointer, size or dtype)";
     case SAF3R_ERR_UNSUPPORTED: return "unsupported (head_dim/block must be 64; size limits)";
-    case SAF3R_ERR_CAPACITY: return "index capacity smaller than saf3r_index_capacity()";
+    case SAF3R_ERR_CAPACITY: return "index capacity or workspace smaller than required";
     case SAF3R_ERR_HIP: return "HIP runtime error on launch";
     case SAF3R_ERR_BAD_TABLE: return "bad pattern table (class or class parameter)";
     default: return "unknown status";

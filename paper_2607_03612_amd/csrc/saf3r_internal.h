@@ -23,6 +23,7 @@ enum Pattern : int32_t {
 
 constexpr int kMaxCosineDim = 4096;   // feature width accepted by the cosine selection
 constexpr int kMaxCosinePerFrame = 64;  // key blocks kept per frame by a cosine head
+constexpr int kNmseParts = 128;         // NMSE partial sums per head (workspace pairs)
 
 // ---------------------------------------------------------------- launches
 
@@ -98,8 +99,8 @@ hipError_t launch_select_global(const double* qp, const double* kpT, int32_t* id
                                 double* scores, const GlobalArgs& a, hipStream_t s);
 hipError_t launch_cosine(int dtype, const void* f, double* fb, double* sim, int32_t* idx,
                          int32_t* cnt, const CosineArgs& a, hipStream_t s);
-hipError_t launch_nmse(int dtype, const void* ref, const void* test, double* out, int heads,
-                       int64_t n, hipStream_t s);
+hipError_t launch_nmse(int dtype, const void* ref, const void* test, void* workspace, double* out,
+                       int heads, int64_t n, hipStream_t s);
 hipError_t launch_attention(int dtype, const void* q, const void* k, const void* v,
                             const int32_t* idx, const int32_t* cnt, void* out, float* lse,
                             const AttnArgs& a, hipStream_t s);

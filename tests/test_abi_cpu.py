@@ -130,7 +130,7 @@ def test_status_strings(B):
     lib = B.load()
     for s in (0, -1, -2, -3, -4, -5, 42):
         assert lib.saf3r_status_string(s)
-    assert lib.saf3r_status_string(-3).decode().startswith("index capacity")
+    assert lib.saf3r_status_string(-3).decode().startswith("index capacity or workspace")
 
 
 def test_cosine_entry_points_validate_before_launch(B):
@@ -157,6 +157,21 @@ def test_cosine_entry_points_validate_before_launch(B):
     assert sel(ctypes.byref(p), t, fake, 0, fake, need, fake, fake, 16, None) == -1
     assert sel(ctypes.byref(p), t, fake, 64, fake, need - 8, fake, fake, 16, None) == -3
     assert sel(ctypes.byref(p), t, fake, 64, fake, need, fake, fake, 15, None) == -3
+
+
+def test_nmse_entry_points_validate_before_launch(B):
+    lib = B.load()
+    p = _p(B, heads=3, frames=8, T=1374)
+    # 128 (numerator, denominator) float64 pairs per head
+    need = lib.saf3r_nmse_workspace_bytes(ctypes.byref(p))
+    assert need == 3 * 128 * 16
+    assert lib.saf3r_nmse_workspace_bytes(None) == -1
+    fake = ctypes.c_void_p(0x1000)  # never dereferenced: validation fails first
+    nm = lib.saf3r_nmse
+    assert nm(ctypes.byref(p), None, fake, fake, need, fake, None) == -1
+    assert nm(ctypes.byref(p), fake, fake, None, need, fake, None) == -1
+    assert nm(ctypes.byref(p), fake, fake, fake, need, None, None) == -1
+    assert nm(ctypes.byref(p), fake, fake, fake, need - 16, fake, None) == -3
 
 
 def test_skip_heads_are_accepted_and_need_nothing(B):
