@@ -327,11 +327,21 @@ saf3r_status saf3r_cosine_select(const saf3r_problem* problem, const saf3r_head_
   a.cap = cap;
   a.dim = feat_dim;
   a.tokens_per_frame = s.tokens_per_frame;
-  for (int h = 0; h < s.heads; ++h) {
-    if (table[h].pattern != SAF3R_COSINE_TOPK) continue;
-    a.head[a.n_heads] = (int16_t)h;
-    a.topk[a.n_heads++] = table[h].param;
+  // the lists depend on the features and the per-frame count only: heads
+  // with equal counts form one group, whose lists are found once
+  std::vector<int> cos;
+  for (int h = 0; h < s.heads; ++h)
+    if (table[h].pattern == SAF3R_COSINE_TOPK) cos.push_back(h);
+  std::stable_sort(cos.begin(), cos.end(),
+                   [&](int x, int y) { return table[x].param < table[y].param; });
+  for (size_t q = 0; q < cos.size(); ++q) {
+    a.head[q] = (int16_t)cos[q];
+    if (q == 0 || table[cos[q]].param != table[cos[q - 1]].param) {
+      a.group_start[a.n_groups] = (int16_t)q;
+      a.group_k[a.n_groups++] = table[cos[q]].param;
+    }
   }
+  a.group_start[a.n_groups] = (int16_t)cos.size();
   double* fb = static_cast<double*>(workspace);
   double* sim = fb + (int64_t)feat_dim * s.nb;
   return hip_status(saf3r::launch_cosine(s.dtype, features, fb, sim, block_idx, block_cnt, a,

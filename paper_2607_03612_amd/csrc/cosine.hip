@@ -10,10 +10,11 @@
 //      unit feature, dimension-major [D][nb];
 //   2. cosine_sim_kernel: the block similarity matrix [nb][nb] as a 64x64
 //      register-tiled product of that matrix with itself;
-//   3. cosine_topk_kernel: one wave per (head, query block); for every frame
-//      (a key block counts under the frame of its first token) it finds the
-//      k-th best (similarity desc, index asc) pair by k passes of a wave-wide
-//      argmax and writes the frame's kept blocks ascending.
+//   3. cosine_topk_kernel: one wave per (per-frame count k, query block), one
+//      lane per frame (a key block counts under the frame of its first
+//      token): k scans find the frame's k-th best (similarity desc, index
+//      asc) pair; the frame's kept blocks go out ascending at an offset from
+//      a prefix sum over the frames, into every head that keeps k per frame.
 // The lists depend on the features only, so they are computed once per
 // sequence and reused by every layer.
 #include "saf3r_internal.h"
@@ -119,75 +120,91 @@ __device__ inline bool ranks_before(double v, int j, double w, int k) {
   return v > w || (v == w && j < k);
 }
 
-// One wave per (cosine head, query block): per-frame Top-K, ascending output.
+// Inclusive prefix sum over the 64 lanes.
+__device__ inline int lane_scan_incl(int v) {
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const int o = __shfl_up(v, d);
+    if ((threadIdx.x & 63) >= d) v += o;
+  }
+  return v;
+}
+
+// One wave per (group of cosine heads with one per-frame count k, query
+// block). Lane f handles frame f (64 frames per pass): k scans of the frame's
+// blocks find its k-th best (similarity desc, index asc) pair, a prefix sum
+// of the per-frame kept counts gives the frame's offset in the row, and the
+// lane writes the frame's kept blocks there in ascending order, into the row
+// of every head of the group.
 __global__ __launch_bounds__(256) void cosine_topk_kernel(const double* __restrict__ sim,
                                                          int32_t* __restrict__ idx,
                                                          int32_t* __restrict__ cnt,
                                                          CosineArgs a) {
   const int lane = threadIdx.x & 63;
   const int64_t wave = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (wave >= (int64_t)a.n_heads * a.nb) return;
-  const int slot = (int)(wave / a.nb);
-  const int i = (int)(wave - (int64_t)slot * a.nb);
-  const int h = a.head[slot];
-  const int k = a.topk[slot];
+  if (wave >= (int64_t)a.n_groups * a.nb) return;
+  const int g = (int)(wave / a.nb);
+  const int i = (int)(wave - (int64_t)g * a.nb);
+  const int k = a.group_k[g];
+  const int q0 = a.group_start[g], q1 = a.group_start[g + 1];
   const double* row = sim + (int64_t)i * a.nb;
-  int32_t* dst = idx + ((int64_t)h * a.nb + i) * a.cap;
   const int64_t T = a.tokens_per_frame;
   const int frames = (int)((a.n + T - 1) / T);
-  int pos = 0;
-  for (int f = 0; f < frames; ++f) {
+  int base = 0;
+  for (int f0 = 0; f0 < frames; f0 += 64) {
     // key blocks whose first token lies in frame f
-    const int j_lo = (int)(((int64_t)f * T + kBlock - 1) / kBlock);
-    const int j_hi = (int)min<int64_t>(((int64_t)(f + 1) * T + kBlock - 1) / kBlock, a.nb);
-    const int size = j_hi - j_lo;
-    if (size <= 0) continue;
-    const int kk = min(k, size);
-    // k-th pair in (value desc, index asc) order: kk passes of a wave argmax
-    // over the pairs ranked after the previous pass's pair
+    const int f = f0 + lane;
+    int j_lo = 0, j_hi = 0;
+    if (f < frames) {
+      j_lo = (int)(((int64_t)f * T + kBlock - 1) / kBlock);
+      j_hi = (int)min<int64_t>(((int64_t)(f + 1) * T + kBlock - 1) / kBlock, a.nb);
+    }
+    const int kk = min(k, max(j_hi - j_lo, 0));
+    // the kk-th pair: each scan takes the best pair ranked after the last
     double tv = __builtin_inf();
     int tj = -1;
     for (int p = 0; p < kk; ++p) {
       double bv = -__builtin_inf();
       int bj = a.nb;
-      for (int j = j_lo + lane; j < j_hi; j += 64) {
+      for (int j = j_lo; j < j_hi; ++j) {
         const double v = row[j];
         if (ranks_before(tv, tj, v, j) && ranks_before(v, j, bv, bj)) {
           bv = v;
           bj = j;
         }
       }
-#pragma unroll
-      for (int m = 32; m >= 1; m >>= 1) {
-        const double ov = __shfl_xor(bv, m);
-        const int oj = __shfl_xor(bj, m);
-        if (ranks_before(ov, oj, bv, bj)) {
-          bv = ov;
-          bj = oj;
-        }
-      }
       tv = bv;
       tj = bj;
     }
-    // the frame's kept blocks: every pair ranked at or before (tv, tj)
-    for (int j0 = j_lo; j0 < j_hi; j0 += 64) {
-      const int j = j0 + lane;
-      const bool keep = j < j_hi && !ranks_before(tv, tj, row[j < j_hi ? j : j_lo], j);
-      const uint64_t m = __ballot(keep);
-      const int at = pos + __popcll(m & ((1ull << lane) - 1));
-      if (keep && at < a.cap) dst[at] = j;
-      pos += __popcll(m);
+    // kept: every pair ranked at or before (tv, tj)
+    int kept = 0;
+    if (kk > 0)
+      for (int j = j_lo; j < j_hi; ++j) kept += ranks_before(tv, tj, row[j], j) ? 0 : 1;
+    const int incl = lane_scan_incl(kept);
+    int pos = base + incl - kept;
+    if (kept > 0) {
+      for (int j = j_lo; j < j_hi; ++j) {
+        if (ranks_before(tv, tj, row[j], j)) continue;
+        if (pos < a.cap)
+          for (int q = q0; q < q1; ++q) idx[((int64_t)a.head[q] * a.nb + i) * a.cap + pos] = j;
+        ++pos;
+      }
     }
+    base += __shfl(incl, 63);
   }
-  for (int p = pos + lane; p < a.cap; p += 64) dst[p] = -1;
-  if (lane == 0) cnt[(int64_t)h * a.nb + i] = pos;
+  for (int q = q0; q < q1; ++q) {
+    const int h = a.head[q];
+    int32_t* dst = idx + ((int64_t)h * a.nb + i) * a.cap;
+    for (int p = base + lane; p < a.cap; p += 64) dst[p] = -1;
+    if (lane == 0) cnt[(int64_t)h * a.nb + i] = base;
+  }
 }
 
 }  // namespace
 
 hipError_t launch_cosine(int dtype, const void* f, double* fb, double* sim, int32_t* idx,
                          int32_t* cnt, const CosineArgs& a, hipStream_t s) {
-  if (a.n_heads == 0) return hipSuccess;
+  if (a.n_groups == 0) return hipSuccess;
   if (dtype == 1)
     hipLaunchKernelGGL(cosine_pool_kernel<uint16_t>, dim3((unsigned)a.nb), dim3(kPoolThreads), 0, s,
                        static_cast<const uint16_t*>(f), fb, a);
@@ -200,7 +217,7 @@ hipError_t launch_cosine(int dtype, const void* f, double* fb, double* sim, int3
   hipLaunchKernelGGL(cosine_sim_kernel, dim3((unsigned)(tiles * tiles)), dim3(256), 0, s, fb, sim, a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const int64_t waves = (int64_t)a.n_heads * a.nb;
+  const int64_t waves = (int64_t)a.n_groups * a.nb;
   hipLaunchKernelGGL(cosine_topk_kernel, dim3((unsigned)((waves + 3) / 4)), dim3(256), 0, s, sim,
                      idx, cnt, a);
   return hipGetLastError();

@@ -85,9 +85,10 @@ struct CosineArgs {
   int32_t cap;
   int32_t dim;  // feature width
   int32_t tokens_per_frame;
-  int32_t n_heads;
+  int32_t n_groups;                     // cosine heads grouped by per-frame count
+  int32_t group_k[kMaxHeads];           // key blocks kept per frame by group g
+  int16_t group_start[kMaxHeads + 1];   // group g: head[group_start[g] .. group_start[g + 1])
   int16_t head[kMaxHeads];
-  int32_t topk[kMaxHeads];  // key blocks kept per frame
 };
 
 hipError_t launch_pool(int dtype, const void* q, const void* k, double* qp, double* kp,

@@ -285,9 +285,14 @@ def _features(n, dim, frames, T, seed):
     return f.astype(np.float32)
 
 
-@pytest.mark.parametrize("frames,T,dtype,dim", [(8, 1374, "bf16", 64), (4, 261, "f32", 96),
-                                                (3, 100, "bf16", 33), (1, 129, "f32", 8)])
-def test_cosine_topk_lists_and_attention(gpu_lib, frames, T, dtype, dim):
+@pytest.mark.parametrize("frames,T,dtype,dim,shared", [(8, 1374, "bf16", 64, False),
+                                                       (4, 261, "f32", 96, True),
+                                                       (3, 100, "bf16", 33, False),
+                                                       (1, 129, "f32", 8, True)])
+def test_cosine_topk_lists_and_attention(gpu_lib, frames, T, dtype, dim, shared):
+    """Cosine lists against the oracle, and attention over them. `shared`:
+    heads 0 and 3 keep the same count per frame (one group, found once and
+    written to both rows) and the group order differs from the head order."""
     import torch
 
     import paper_2607_03612_amd as P
@@ -301,7 +306,10 @@ def test_cosine_topk_lists_and_attention(gpu_lib, frames, T, dtype, dim):
     else:
         f_in = f32
     f64 = O.to_f64(f_in, dtype)
-    table = [(O.COSINE_TOPK, 1), (O.COSINE_TOPK, 3), (O.TOPK, max(1, w.nb // 4)), (O.DENSE, 0)]
+    if shared:
+        table = [(O.COSINE_TOPK, 3), (O.COSINE_TOPK, 1), (O.TOPK, max(1, w.nb // 4)), (O.COSINE_TOPK, 3)]
+    else:
+        table = [(O.COSINE_TOPK, 1), (O.COSINE_TOPK, 3), (O.TOPK, max(1, w.nb // 4)), (O.DENSE, 0)]
     tq, tk, tv = (PT.to_device(x, dtype) for x in (q, k, v))
     code = P.BF16 if dtype == "bf16" else P.F32
     cap = P.index_capacity(table, frames, T, code)
@@ -325,6 +333,36 @@ def test_cosine_topk_lists_and_attention(gpu_lib, frames, T, dtype, dim):
         assert PT.max_abs(res["out"][h], ref["out"][h]) <= tol, h
         assert PT.max_abs(res["lse"][h], ref["lse"][h]) <= lse_tol, h
     print(f"[parity] cosine {w.name}: near-ties {near}", flush=True)
+
+
+@pytest.mark.parametrize("frames,T,ks", [(70, 261, (1, 4, 1)), (130, 130, (2, 1, 64))])
+def test_cosine_lists_many_frames(gpu_lib, frames, T, ks):
+    """Cosine lists only (no attention) with more frames than lanes: 70 and
+    130 frames take two and three passes of 64 frames per wave; two heads
+    share a count, a SKIP head keeps its rows, and k = 64 keeps every block
+    of a frame."""
+    import torch
+
+    import paper_2607_03612_amd as P
+
+    w = Workload(f"cosl-{frames}x{T}", frames, T, "f32", ("fixed", 1, 1, 50), heads=4)
+    q, k, _ = make_qkv(w)
+    f_in = _features(w.tokens, 16, frames, T, seed=frames)
+    table = [(O.COSINE_TOPK, ks[0]), (O.COSINE_TOPK, ks[1]), (P.SKIP, 0), (O.COSINE_TOPK, ks[2])]
+    cap = P.index_capacity(table, frames, T, P.F32)
+    idx = torch.full((4, w.nb, cap), -7, dtype=torch.int32, device="cuda")
+    cnt = torch.full((4, w.nb), -9, dtype=torch.int32, device="cuda")
+    P.cosine_select(PT.to_device(f_in, "f32"), table, frames, T, idx, cnt)
+    torch.cuda.synchronize()
+    res = {"idx": idx.cpu().numpy(), "cnt": cnt.cpu().numpy()}
+    assert (res["idx"][2] == -7).all() and (res["cnt"][2] == -9).all()
+    cos_table = [t if t[0] != P.SKIP else (O.DENSE, 0) for t in table]
+    ref = O.run_layer(q, k, k, cos_table, T, "f32", features=O.to_f64(f_in, "f32"),
+                      with_attention=False)
+    for h in (0, 1, 3):
+        for i in range(w.nb):
+            PT.check_lists(res, h, i, O.COSINE_TOPK, ref["lists"][h][i], ref["margins"][h][i],
+                           w.nb, cap)
 
 
 # ------------------------------------------------- NMSE and the profiler
