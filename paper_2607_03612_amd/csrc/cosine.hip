@@ -9,7 +9,8 @@
 //   1. cosine_pool_kernel: one workgroup per block writes the block's mean
 //      unit feature, dimension-major [D][nb];
 //   2. cosine_sim_kernel: the block similarity matrix [nb][nb] as a 64x64
-//      register-tiled product of that matrix with itself;
+//      register-tiled product of that matrix with itself (upper tiles only,
+//      mirrored);
 //   3. cosine_topk_kernel: one wave per (per-frame count k, query block), one
 //      lane per frame (a key block counts under the frame of its first
 //      token): k scans find the frame's k-th best (similarity desc, index
@@ -36,43 +37,81 @@ __device__ inline double feat_at<float>(const float* f, int64_t i) {
 }
 
 // Mean unit feature of block b: fb[d][b] = (1/n_b) sum_t f[t][d] / |f[t]|.
-template <typename T>
+// kVec: rows are whole 16-byte vectors (feat_dim * element size a multiple
+// of 16, 16-byte aligned base), read 16 bytes per lane; otherwise one element
+// per lane.
+template <typename T, bool kVec>
 __global__ __launch_bounds__(kPoolThreads) void cosine_pool_kernel(const T* __restrict__ f,
                                                                   double* __restrict__ fb,
                                                                   CosineArgs a) {
+  constexpr int kPer = 16 / (int)sizeof(T);  // elements per 16-byte vector
   __shared__ double inv_norm[kBlock];
-  __shared__ double part[kPoolThreads / 64];
   const int b = blockIdx.x;
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const int64_t row0 = (int64_t)b * kBlock;
   const int rows = (int)min<int64_t>(kBlock, a.n - row0);
+  const int vecs = a.dim / kPer;  // 16-byte vectors per row (kVec)
   // 1/|f_t| for the block's tokens: one wave per token
   for (int r = wave; r < rows; r += kPoolThreads / 64) {
     double ss = 0.0;
-    for (int d = lane; d < a.dim; d += 64) {
-      const double x = feat_at(f, (row0 + r) * a.dim + d);
-      ss = fma(x, x, ss);
+    if constexpr (kVec) {
+      const uint4* row = reinterpret_cast<const uint4*>(f + (row0 + r) * a.dim);
+      for (int c = lane; c < vecs; c += 64) {
+        const uint4 u = row[c];
+        const T* e = reinterpret_cast<const T*>(&u);
+#pragma unroll
+        for (int q = 0; q < kPer; ++q) {
+          const double x = feat_at(e, q);
+          ss = fma(x, x, ss);
+        }
+      }
+    } else {
+      for (int d = lane; d < a.dim; d += 64) {
+        const double x = feat_at(f, (row0 + r) * a.dim + d);
+        ss = fma(x, x, ss);
+      }
     }
 #pragma unroll
     for (int m = 32; m >= 1; m >>= 1) ss += __shfl_xor(ss, m);
     if (lane == 0) inv_norm[r] = 1.0 / sqrt(ss);
   }
   __syncthreads();
-  for (int d = t; d < a.dim; d += kPoolThreads) {
-    double acc = 0.0;
-    for (int r = 0; r < rows; ++r) acc = fma(feat_at(f, (row0 + r) * a.dim + d), inv_norm[r], acc);
-    fb[(int64_t)d * a.nb + b] = acc / (double)rows;
+  if constexpr (kVec) {
+    // thread t: dimensions [kPer c, kPer c + kPer) for c = t, t + 256, ...
+    for (int c = t; c < vecs; c += kPoolThreads) {
+      double acc[kPer];
+#pragma unroll
+      for (int q = 0; q < kPer; ++q) acc[q] = 0.0;
+      const uint4* col = reinterpret_cast<const uint4*>(f + row0 * a.dim) + c;
+      for (int r = 0; r < rows; ++r) {
+        const uint4 u = col[(int64_t)r * vecs];
+        const T* e = reinterpret_cast<const T*>(&u);
+#pragma unroll
+        for (int q = 0; q < kPer; ++q) acc[q] = fma(feat_at(e, q), inv_norm[r], acc[q]);
+      }
+#pragma unroll
+      for (int q = 0; q < kPer; ++q) fb[(int64_t)(kPer * c + q) * a.nb + b] = acc[q] / (double)rows;
+    }
+  } else {
+    for (int d = t; d < a.dim; d += kPoolThreads) {
+      double acc = 0.0;
+      for (int r = 0; r < rows; ++r) acc = fma(feat_at(f, (row0 + r) * a.dim + d), inv_norm[r], acc);
+      fb[(int64_t)d * a.nb + b] = acc / (double)rows;
+    }
   }
-  (void)part;
 }
 
 // sim[i][j] = sum_d fb[d][i] fb[d][j]: 64x64 tiles, 16x16 threads of 4x4.
+// The matrix is symmetric: only tiles on or above the diagonal are computed,
+// and an off-diagonal tile is also stored transposed (the same fma sequence
+// with the two factors swapped, so the same bits).
 __global__ __launch_bounds__(256) void cosine_sim_kernel(const double* __restrict__ fb,
                                                         double* __restrict__ sim, CosineArgs a) {
   __shared__ double as[16][64];
   __shared__ double bs[16][64];
   const int tiles = (a.nb + 63) / 64;
   const int ti = blockIdx.x / tiles, tj = blockIdx.x - (blockIdx.x / tiles) * tiles;
+  if (ti > tj) return;
   const int i0 = ti * 64, j0 = tj * 64;
   const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
   double acc[4][4];
@@ -110,7 +149,10 @@ __global__ __launch_bounds__(256) void cosine_sim_kernel(const double* __restric
 #pragma unroll
     for (int y = 0; y < 4; ++y) {
       const int j = j0 + 4 * tx + y;
-      if (j < a.nb) sim[(int64_t)i * a.nb + j] = acc[x][y];
+      if (j < a.nb) {
+        sim[(int64_t)i * a.nb + j] = acc[x][y];
+        if (ti != tj) sim[(int64_t)j * a.nb + i] = acc[x][y];
+      }
     }
   }
 }
@@ -205,12 +247,22 @@ __global__ __launch_bounds__(256) void cosine_topk_kernel(const double* __restri
 hipError_t launch_cosine(int dtype, const void* f, double* fb, double* sim, int32_t* idx,
                          int32_t* cnt, const CosineArgs& a, hipStream_t s) {
   if (a.n_groups == 0) return hipSuccess;
-  if (dtype == 1)
-    hipLaunchKernelGGL(cosine_pool_kernel<uint16_t>, dim3((unsigned)a.nb), dim3(kPoolThreads), 0, s,
-                       static_cast<const uint16_t*>(f), fb, a);
-  else
-    hipLaunchKernelGGL(cosine_pool_kernel<float>, dim3((unsigned)a.nb), dim3(kPoolThreads), 0, s,
-                       static_cast<const float*>(f), fb, a);
+  const int esz = dtype == 1 ? 2 : 4;
+  const bool vec = ((int64_t)a.dim * esz) % 16 == 0 && (reinterpret_cast<uintptr_t>(f) & 15) == 0;
+  const dim3 grid((unsigned)a.nb), block(kPoolThreads);
+  if (dtype == 1) {
+    const uint16_t* fp = static_cast<const uint16_t*>(f);
+    if (vec)
+      hipLaunchKernelGGL((cosine_pool_kernel<uint16_t, true>), grid, block, 0, s, fp, fb, a);
+    else
+      hipLaunchKernelGGL((cosine_pool_kernel<uint16_t, false>), grid, block, 0, s, fp, fb, a);
+  } else {
+    const float* fp = static_cast<const float*>(f);
+    if (vec)
+      hipLaunchKernelGGL((cosine_pool_kernel<float, true>), grid, block, 0, s, fp, fb, a);
+    else
+      hipLaunchKernelGGL((cosine_pool_kernel<float, false>), grid, block, 0, s, fp, fb, a);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int tiles = (a.nb + 63) / 64;
