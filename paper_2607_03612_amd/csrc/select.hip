@@ -532,7 +532,8 @@ __global__ __launch_bounds__(kStaticThreads) void select_static_kernel(int32_t* 
   if (lane == 0) cnt[row] = len;
 }
 
-constexpr int kGlobalThreads = 256;
+constexpr int kGlobalThreads = 1024;
+constexpr int kGlobalWaves = kGlobalThreads / 64;
 
 // One workgroup per global-probe head; writes row 0 of the head's lists.
 __global__ __launch_bounds__(kGlobalThreads) void select_global_kernel(const double* __restrict__ qp,
@@ -542,10 +543,10 @@ __global__ __launch_bounds__(kGlobalThreads) void select_global_kernel(const dou
                                                                       double* __restrict__ scores,
                                                                       GlobalArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint64_t skeys[];  // [nb] order keys
-  __shared__ double part[kGlobalThreads / 64][kHeadDim];
+  __shared__ double part[kGlobalWaves][kHeadDim];
   __shared__ double qbar[kHeadDim];
   __shared__ uint32_t hist[256];
-  __shared__ uint32_t wave_tot[kGlobalThreads / 64][2];
+  __shared__ uint32_t wave_tot[kGlobalWaves][2];
   __shared__ int sel_digit, sel_above;
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const int h = a.head[blockIdx.x];
@@ -554,27 +555,44 @@ __global__ __launch_bounds__(kGlobalThreads) void select_global_kernel(const dou
   const double* qh = qp + (int64_t)h * nb * kHeadDim;
   const double* kT = kpT + (int64_t)h * kHeadDim * nb;
 
-  // probe: mean of all queries = sum over blocks of (block size) * block mean, over N
-  double acc = 0.0;
-  for (int b = wave; b < nb; b += kGlobalThreads / 64) {
-    const double nbk = b == nb - 1 ? (double)(a.n - (int64_t)(nb - 1) * kBlock) : (double)kBlock;
-    acc = fma(nbk, qh[(int64_t)b * kHeadDim + lane], acc);
+  // probe: mean of all queries = sum over blocks of (block size) * block mean,
+  // over N. Wave w sums blocks w, w + 16, ... in two interleaved chains; the
+  // partial sums are added in a fixed order.
+  double acc0 = 0.0, acc1 = 0.0;
+  int b = wave;
+  for (; b + 7 * kGlobalWaves < nb; b += 8 * kGlobalWaves) {
+    double x[8];  // eight loads in flight, then the two chains
+#pragma unroll
+    for (int u = 0; u < 8; ++u) x[u] = qh[(int64_t)(b + u * kGlobalWaves) * kHeadDim + lane];
+#pragma unroll
+    for (int u = 0; u < 8; u += 2) {
+      acc0 = fma((double)kBlock, x[u], acc0);
+      const int b1 = b + (u + 1) * kGlobalWaves;
+      const double n1 = b1 == nb - 1 ? (double)(a.n - (int64_t)(nb - 1) * kBlock) : (double)kBlock;
+      acc1 = fma(n1, x[u + 1], acc1);
+    }
   }
-  part[wave][lane] = acc;
+  for (; b < nb; b += kGlobalWaves) {
+    const double n0 = b == nb - 1 ? (double)(a.n - (int64_t)(nb - 1) * kBlock) : (double)kBlock;
+    acc0 = fma(n0, qh[(int64_t)b * kHeadDim + lane], acc0);
+  }
+  part[wave][lane] = acc0 + acc1;
   __syncthreads();
   if (t < kHeadDim) {
     double sum = 0.0;
 #pragma unroll
-    for (int w = 0; w < kGlobalThreads / 64; ++w) sum += part[w][t];
+    for (int w = 0; w < kGlobalWaves; ++w) sum += part[w][t];
     qbar[t] = sum / (double)a.n;
   }
   __syncthreads();
 
-  // scores of every key block, in float64, kept as order keys
+  // scores of every key block, in float64 (four interleaved chains over the
+  // dimensions, added in a fixed order), kept as order keys
   for (int j = t; j < nb; j += kGlobalThreads) {
-    double sj = 0.0;
-    for (int d = 0; d < kHeadDim; ++d) sj = fma(qbar[d], kT[(int64_t)d * nb + j], sj);
-    sj *= 0.125;  // 1/sqrt(64), exact
+    double s4[4] = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+    for (int d = 0; d < kHeadDim; ++d) s4[d & 3] = fma(qbar[d], kT[(int64_t)d * nb + j], s4[d & 3]);
+    const double sj = ((s4[0] + s4[1]) + (s4[2] + s4[3])) * 0.125;  // 1/sqrt(64), exact
     skeys[j] = order_key(sj);
     if (scores) scores[(int64_t)h * nb * nb + j] = sj;
   }
@@ -584,21 +602,35 @@ __global__ __launch_bounds__(kGlobalThreads) void select_global_kernel(const dou
   uint64_t prefix = 0, mask = 0;
   int remaining = k;
   for (int shift = 56; shift >= 0; shift -= 8) {
-    hist[t] = 0;  // kGlobalThreads == 256 bins
+    if (t < 256) hist[t] = 0;
     __syncthreads();
     for (int j = t; j < nb; j += kGlobalThreads) {
       const uint64_t key = skeys[j];
       if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255], 1u);
     }
     __syncthreads();
-    if (t == 0) {
-      int above = 0, d = 255;
-      for (; d > 0; --d) {
-        if (above + (int)hist[d] >= remaining) break;
-        above += (int)hist[d];
+    // digit of the k-th key: the first d, from 255 down, at which the count
+    // of keys with digit >= d reaches `remaining` (a scan over the bins in
+    // descending order by the first four waves; digit 0 if none does)
+    if (t < 256) {
+      const uint32_t hv = hist[255 - t];
+      const uint32_t incl = wave_scan_incl(hv);
+      if (lane == 63) wave_tot[wave][0] = incl;
+    }
+    __syncthreads();
+    if (t < 256) {
+      const uint32_t hv = hist[255 - t];
+      uint32_t incl = wave_scan_incl(hv);
+      for (int w = 0; w < wave; ++w) incl += wave_tot[w][0];
+      const bool reach = (int)incl >= remaining;
+      const uint32_t prev = incl - hv;
+      // the first lane (lowest t) that reaches; t = 255 (digit 0) always takes
+      // the rest
+      const bool first = (reach && (int)prev < remaining) || (t == 255 && (int)prev < remaining && !reach);
+      if (first) {
+        sel_digit = 255 - t;
+        sel_above = (int)prev;
       }
-      sel_digit = d;
-      sel_above = above;
     }
     __syncthreads();
     prefix |= (uint64_t)sel_digit << shift;
@@ -630,7 +662,7 @@ __global__ __launch_bounds__(kGlobalThreads) void select_global_kernel(const dou
     if (kept && pos < a.cap) dst[pos] = j;
     int eq_chunk = 0, kept_chunk = 0;
 #pragma unroll
-    for (int w = 0; w < kGlobalThreads / 64; ++w) {
+    for (int w = 0; w < kGlobalWaves; ++w) {
       eq_chunk += (int)wave_tot[w][0];
       kept_chunk += (int)wave_tot[w][1];
     }

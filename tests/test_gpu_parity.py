@@ -250,6 +250,24 @@ def test_global_probe_gives_every_query_block_one_list(gpu_lib):
         np.testing.assert_array_equal(rows[0], sel)
 
 
+def test_equal_scores_keep_the_lowest_block_indices(gpu_lib):
+    """Every key token equal: all block scores are the same float64 value, so
+    the Top-K and global-probe selections reduce to the tie rule of the
+    oracle's stable sort (lowest block indices first). This drives the Top-K
+    kernel through its tie-bucket refinement over the whole row and the radix
+    select through a single bucket at every digit."""
+    import paper_2607_03612_amd as P
+
+    w = Workload("ties-3x261", 3, 261, "bf16", ("fixed", 1, 1, 50), heads=3)
+    q, k, v = make_qkv(w)
+    k[:] = k[0, 0]  # one key vector for every head and token
+    table = [(O.GLOBAL_PROBE, 5), (O.TOPK, 7), (O.TOPK, w.nb - 1)]
+    res = PT.gpu_layer(P, w, q, k, v, table, want_lse=False)
+    for h, kk in enumerate((5, 7, w.nb - 1)):
+        assert np.all(res["cnt"][h] == kk), h
+        np.testing.assert_array_equal(res["idx"][h, :, :kk], np.tile(np.arange(kk), (w.nb, 1)))
+
+
 @pytest.mark.parametrize("stride", [8, 33])
 def test_stride_sampled_parity_large(gpu_lib, stride):
     """The 137400-token layer with STRIDE heads, checked on sampled query
