@@ -2,8 +2,8 @@
 // of queries is their mean; SAF3R's online stage pools every 64-token block of
 // Q and K of each Top-K head.
 //
-// HBM-bound: each 64x64 tile is read once with 16-byte coalesced loads (one
-// wave per tile, eight rows of 128 B per load instruction) and summed in
+// HBM-bound: each 64x64 tile is read once with 16-byte coalesced nontemporal
+// loads (one wave per tile, eight rows of 128 B per load instruction) and summed in
 // float64, which is exact for bf16 inputs (8-bit significands summed in a
 // 53-bit significand), then divided by the block's own token count. Pooled Q
 // is written [H][nb][64]; pooled K dimension-major [H][64][nb], the layout
@@ -14,6 +14,8 @@ namespace saf3r {
 namespace {
 
 constexpr int kWavesPerGroup = 4;
+
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 __device__ inline float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ inline float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
@@ -40,26 +42,28 @@ __global__ __launch_bounds__(256) void pool_bf16_kernel(const uint16_t* __restri
   const int c = lane & 7;   // 16-byte chunk = 8 columns
 
   // rows past a partial last block load a clamped valid row (so all eight
-  // loads issue back to back) and are zeroed afterwards
-  uint4 v[8];
+  // loads issue back to back) and are zeroed afterwards; the loads are
+  // nontemporal (each tile is read once here), which keeps them from
+  // displacing other lines and makes the stream faster from a cold cache
+  u32x4 v[8];
 #pragma unroll
   for (int it = 0; it < 8; ++it) {
     const int row = r + 8 * it;
-    v[it] = *reinterpret_cast<const uint4*>(src + min(row, rows - 1) * kHeadDim + c * 8);
+    v[it] = __builtin_nontemporal_load(
+        reinterpret_cast<const u32x4*>(src + min(row, rows - 1) * kHeadDim + c * 8));
   }
 #pragma unroll
   for (int it = 0; it < 8; ++it)
-    if (r + 8 * it >= rows) v[it] = make_uint4(0, 0, 0, 0);
+    if (r + 8 * it >= rows) v[it] = u32x4{0u, 0u, 0u, 0u};
   double acc[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) acc[e] = 0.0;
 #pragma unroll
   for (int it = 0; it < 8; ++it) {
-    const uint32_t w4[4] = {v[it].x, v[it].y, v[it].z, v[it].w};
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      acc[2 * e] += (double)bf16_lo(w4[e]);
-      acc[2 * e + 1] += (double)bf16_hi(w4[e]);
+      acc[2 * e] += (double)bf16_lo(v[it][e]);
+      acc[2 * e + 1] += (double)bf16_hi(v[it][e]);
     }
   }
   // lanes c, c+8, ..., c+56 hold partial sums of the same 8 columns
