@@ -117,9 +117,12 @@ def blas_threads():
 
 
 def event_ms(torch, fn, reps):
-    """Mean milliseconds of ``fn`` over ``reps`` launches (one untimed first)."""
+    """Mean milliseconds of ``fn`` over ``reps`` launches. An untimed first
+    launch is still running when the start event is queued, so the timed
+    launches follow it back to back without host latency."""
     fn()
     torch.cuda.synchronize()
+    fn()
     a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     a.record()
     for _ in range(reps):
@@ -309,10 +312,13 @@ def main():
     sink = torch.zeros((), dtype=torch.float32, device=dev)
 
     def cold_ms(fn, reps=5):
+        # The flush is queued on the same stream and the host does not wait
+        # for it: the start event fires when the flush ends, by which time the
+        # timed launch is already queued, so host launch latency stays out.
         ts = []
         for _ in range(reps):
-            sink.copy_(flush_buf.sum())
             torch.cuda.synchronize()
+            sink.copy_(flush_buf.sum())
             a0, a1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             a0.record()
             fn()
