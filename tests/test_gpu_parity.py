@@ -110,6 +110,19 @@ def test_sampled_parity_large(gpu_lib, name, layer):
     _sampled_check(P, WORKLOADS[name], layer, samples=24, seed=layer + 1)
 
 
+def test_maximum_size_sampled(gpu_lib):
+    """The largest problem the library accepts: N = 1048576 tokens (16384
+    blocks) in 8 frames of 131072 tokens, two Top-K heads (k = 164) and one
+    frame-local head (2048-block frames). Top-K scoring then runs two rows
+    per workgroup and the row-in-LDS selection path; sampled rows against
+    the oracle."""
+    import paper_2607_03612_amd as P
+
+    w = Workload("max-8x131072", 8, 131072, "bf16", ("fixed", 0, 1, 1), heads=3)
+    assert w.tokens == 1 << 20 and w.nb == 16384
+    _sampled_check(P, w, 0, samples=6, seed=11)
+
+
 # ------------------------------------------------------------ edge cases
 
 EDGE = [
