@@ -236,6 +236,21 @@ def test_all_classes_full_parity(gpu_lib, frames, T, dtype):
     print(f"[parity] {w.name}: near-ties {near}", flush=True)
 
 
+def test_maximum_head_count_full_parity(gpu_lib):
+    """256 heads, the most the library accepts, cycling through every class
+    on a small ragged layer (3 frames x 100 tokens): per-class launches,
+    the cost ordering of the list heads and the head indices carried in
+    the kernel arguments all run at their limits."""
+    import paper_2607_03612_amd as P
+
+    w = Workload("heads256-3x100-bf16", 3, 100, "bf16", ("fixed", 1, 1, 50), heads=256)
+    q, k, v = make_qkv(w)
+    base = _all_classes_table(w)
+    table = [base[h % len(base)] for h in range(256)]
+    _, _, near = _full_check(P, w, q, k, v, table, want_scores=False)
+    print(f"[parity] {w.name}: near-ties {near}", flush=True)
+
+
 def test_stride_one_equals_dense_bitwise(gpu_lib):
     import paper_2607_03612_amd as P
 
