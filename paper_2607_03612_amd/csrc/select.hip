@@ -8,7 +8,8 @@
 // operand and the dimension-major pooled keys as coalesced B columns. Scores
 // become order-preserving 64-bit keys; LDS keeps only their high 32 bits.
 // One wave per query block then, with its row of high keys in registers (lane
-// l holds blocks [l*C, l*C + C), C = ceil(nb / 64)):
+// l holds blocks [l*C, l*C + C), C = ceil(nb / 64) rounded up to a multiple
+// of 4, read as 16-byte LDS words):
 //   1. brackets the k-th largest high key between two pivots read off a
 //      stratified sample (one key per lane), checks the bracket with one
 //      counting pass and, once it holds at most 512 keys, packs those into
@@ -117,9 +118,17 @@ __device__ inline f64x4 score_tile(const QOperand& q, const KColumn& k) {
   return a0 + a1;
 }
 
-// Row of high keys of one query block; lane l owns blocks l*C + e, e < C.
-// Held in registers when C <= MAXK (MAXK > 0), else read from LDS on every
-// pass. Slots past the last block hold 0, below every valid key.
+// Row of high keys of one query block; lane l owns blocks l*C + e, e < C,
+// with C = ceil(nb / 64) rounded up to a multiple of 4 so that a lane's
+// chunk is whole 16-byte LDS words. Held in registers when C <= MAXK
+// (MAXK > 0), else read from LDS on every pass. Slots past the last block
+// hold 0, below every valid key.
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// Key slots per lane for a row of nb blocks: ceil(nb / 64) rounded up to a
+// multiple of 4; a row occupies 64 * row_chunk(nb) words of LDS.
+__host__ __device__ inline int row_chunk(int nb) { return ((nb + 63) / 64 + 3) & ~3; }
+
 template <int MAXK>
 struct RowKeys {
   uint32_t r[MAXK > 0 ? MAXK : 1];
@@ -129,18 +138,22 @@ struct RowKeys {
   __device__ inline void init(const uint32_t* row, int nb_, int lane) {
     lds = row;
     nb = nb_;
-    C = (nb + 63) / 64;
+    C = row_chunk(nb);
     base = lane * C;
     if constexpr (MAXK > 0) {
+      static_assert(MAXK % 4 == 0, "slots are read four at a time");
 #pragma unroll
       for (int e = 0; e < MAXK; ++e) r[e] = 0u;
-      // reads up to 64*C + 6 entries past the row start: the LDS holds
-      // kRowPad slack entries after the last row; slots e >= C belong to no
-      // block
-      each_slot([&](int e) {
-        const uint32_t x = row[base + e];
-        r[e] = e < C && base + e < nb ? x : 0u;
-      });
+      // the lane's chunk as 16-byte LDS reads (rows are 64*C words long)
+      const u32x4* src = reinterpret_cast<const u32x4*>(row + base);
+#pragma unroll
+      for (int q = 0; q < MAXK / 4; ++q) {
+        if (4 * q < C) {
+          const u32x4 x = src[q];
+#pragma unroll
+          for (int t = 0; t < 4; ++t) r[4 * q + t] = base + 4 * q + t < nb ? x[t] : 0u;
+        }
+      }
     }
   }
   // g(e) for every slot e < C, in groups of 8 behind one uniform branch
@@ -228,7 +241,8 @@ __global__ __launch_bounds__(THREADS) void select_topk_kernel(const double* __re
   const int h = a.head[slot];
   const int k = a.topk[slot];
 
-  uint32_t* keys = reinterpret_cast<uint32_t*>(lds);  // [R][nb] high halves
+  uint32_t* keys = reinterpret_cast<uint32_t*>(lds);  // [R][ld] high halves
+  const int ld = 64 * row_chunk(nb);
 
   // ---- scores: 16x16 fp64 MFMA tiles, one chunk of 16 key blocks per step
   const int lane = threadIdx.x & 63;
@@ -249,7 +263,7 @@ __global__ __launch_bounds__(THREADS) void select_topk_kernel(const double* __re
         const int r = (lane >> 4) + 4 * e;
         if (r < rows && j < nb) {
           const double s = t[e] * 0.125;  // 1/sqrt(64), exact
-          keys[r * nb + j] = (uint32_t)(order_key(s) >> 32);
+          keys[r * ld + j] = (uint32_t)(order_key(s) >> 32);
           if (scores) scores[((int64_t)h * nb + i0 + r) * nb + j] = s;
         }
       }
@@ -260,7 +274,7 @@ __global__ __launch_bounds__(THREADS) void select_topk_kernel(const double* __re
   // ---- selection: one wave per query block
   constexpr int kMaskWords = MAXK > 0 ? 1 : 4;  // C <= 48, or <= 256 (nb <= 16384)
   for (int r = wave; r < rows; r += kWaves) {
-    uint32_t* lrow = keys + r * nb;
+    uint32_t* lrow = keys + r * ld;
     int32_t* dst = idx + ((int64_t)h * nb + i0 + r) * a.cap;
     RowKeys<MAXK> row;
     row.init(lrow, nb, lane);
@@ -708,7 +722,7 @@ hipError_t launch_topk(const double* qp, const double* kpT, int32_t* idx, int32_
 template <int R, int THREADS>
 hipError_t launch_topk_rows(const double* qp, const double* kpT, int32_t* idx, int32_t* cnt,
                             double* scores, const TopKArgs& a, size_t lds, hipStream_t s) {
-  const int chunks = (a.nb + 63) / 64;
+  const int chunks = row_chunk(a.nb);
   if (chunks <= 4) return launch_topk<R, THREADS, 4>(qp, kpT, idx, cnt, scores, a, lds, s);
   if (chunks <= 16) return launch_topk<R, THREADS, 16>(qp, kpT, idx, cnt, scores, a, lds, s);
   if (chunks <= 48) return launch_topk<R, THREADS, 48>(qp, kpT, idx, cnt, scores, a, lds, s);
@@ -718,7 +732,7 @@ hipError_t launch_topk_rows(const double* qp, const double* kpT, int32_t* idx, i
 }  // namespace
 
 size_t topk_lds_bytes(int rows, int nb) {
-  return ((size_t)rows * nb + kRowPad) * sizeof(uint32_t);
+  return ((size_t)rows * 64 * row_chunk(nb) + kRowPad) * sizeof(uint32_t);
 }
 
 int topk_threads(int rows) { return rows >= 16 ? 512 : 256; }
