@@ -241,6 +241,10 @@ def main():
     idx = torch.empty((H, nb, cap), dtype=torch.int32, device=dev)
     cnt = torch.empty((H, nb), dtype=torch.int32, device=dev)
     out = torch.empty_like(tq)
+    # Top-K scores go through a workspace (two launches, faster than the
+    # single launch that keeps score rows in LDS; the same lists)
+    sel_ws_bytes = P.select_workspace_bytes(table, S, T, code)
+    sel_ws = torch.empty(max(sel_ws_bytes, 16) // 4, dtype=torch.int32, device=dev)
 
     def step(ev=None):
         if ev:
@@ -248,7 +252,7 @@ def main():
         P.estimate_blocks(tq, tk, table, S, T, qp, kp)
         if ev:
             ev[1].record()
-        P.select_blocks(qp, kp, table, S, T, cap, idx, cnt, dtype=code)
+        P.select_blocks(qp, kp, table, S, T, cap, idx, cnt, dtype=code, workspace=sel_ws)
         if ev:
             ev[2].record()
         P.sparse_attention(tq, tk, tv, table, S, T, idx, cnt, out)

@@ -158,11 +158,29 @@ saf3r_status saf3r_estimate_blocks(const saf3r_problem* problem, const saf3r_hea
  *   scores_or_null     NULL, or device float64 [heads, nb, nb]: the full score
  *                      matrix of every TOPK head; for a GLOBAL_PROBE head the
  *                      probe scores in row 0 (other rows and heads untouched)
- * Returns SAF3R_OK, or an error with nothing enqueued. */
+ *   workspace_or_null  NULL: the TOPK rows are scored and selected in one
+ *                      launch whose workgroups keep 16 score rows in LDS (the
+ *                      library allocates nothing). Otherwise device memory,
+ *                      16-byte aligned, of workspace_bytes bytes, overwritten:
+ *                      the TOPK scores go there as one launch, and a second
+ *                      selects one row per wave at higher occupancy (faster).
+ *                      It must hold at least one TOPK head's share,
+ *                      saf3r_select_workspace_bytes / (number of TOPK heads);
+ *                      with less than the full size the heads are done in
+ *                      batches. Both ways give the same lists.
+ * Returns SAF3R_OK; SAF3R_ERR_CAPACITY for a cap or a workspace too small;
+ * another error code with nothing enqueued. */
 saf3r_status saf3r_select_blocks(const saf3r_problem* problem, const saf3r_head_cfg* table,
                                  const double* q_pooled, const double* k_pooled,
                                  int32_t* block_idx, int32_t* block_cnt, int32_t cap,
-                                 double* scores_or_null, void* stream);
+                                 double* scores_or_null, void* workspace_or_null,
+                                 int64_t workspace_bytes, void* stream);
+
+/* Workspace of saf3r_select_blocks that takes every TOPK head in one batch:
+ * (TOPK heads) x nb x 64 x C x 4 bytes, C = ceil(nb / 64) rounded up to a
+ * multiple of 4 (198 MB for 10 TOPK heads at nb = 2147); 0 without TOPK
+ * heads; or a negative saf3r_status. */
+int64_t saf3r_select_workspace_bytes(const saf3r_problem* problem, const saf3r_head_cfg* table);
 
 /* Attention restricted to the kept keys (Sec. 4.1: compute only the scores
  * between the queries and the selected keys, softmax renormalised over

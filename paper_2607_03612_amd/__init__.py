@@ -24,6 +24,7 @@ from .binding import (  # noqa: F401
     num_blocks,
     run_layer,
     select_blocks,
+    select_workspace_bytes,
     SKIP,
     sparse_attention,
     STRIDE,

@@ -22,6 +22,7 @@ EXPORTS = (
     "saf3r_index_capacity",
     "saf3r_estimate_blocks",
     "saf3r_select_blocks",
+    "saf3r_select_workspace_bytes",
     "saf3r_sparse_attention",
     "saf3r_cosine_workspace_bytes",
     "saf3r_cosine_select",
@@ -58,8 +59,10 @@ def _declare(lib):
     lib.saf3r_index_capacity.restype = I32
     lib.saf3r_estimate_blocks.argtypes = [P, C, V, V, V, V, V]
     lib.saf3r_estimate_blocks.restype = I32
-    lib.saf3r_select_blocks.argtypes = [P, C, V, V, V, V, I32, V, V]
+    lib.saf3r_select_blocks.argtypes = [P, C, V, V, V, V, I32, V, V, ctypes.c_int64, V]
     lib.saf3r_select_blocks.restype = I32
+    lib.saf3r_select_workspace_bytes.argtypes = [P, C]
+    lib.saf3r_select_workspace_bytes.restype = ctypes.c_int64
     lib.saf3r_sparse_attention.argtypes = [P, C, V, V, V, V, V, I32, V, V, V]
     lib.saf3r_sparse_attention.restype = I32
     lib.saf3r_cosine_workspace_bytes.argtypes = [P, I32]
@@ -177,9 +180,23 @@ def estimate_blocks(q, k, table, frames, tokens_per_frame, q_pooled=None, k_pool
     return q_pooled, k_pooled
 
 
+def select_workspace_bytes(table, frames, tokens_per_frame, dtype=BF16) -> int:
+    """Bytes of the workspace that lets saf3r_select_blocks take every TOPK
+    head in one batch (0 without TOPK heads)."""
+    p = problem(len(table), frames, tokens_per_frame, dtype)
+    r = _lib().saf3r_select_workspace_bytes(ctypes.byref(p), head_table(table))
+    _check(min(r, 0), "saf3r_select_workspace_bytes")
+    return int(r)
+
+
 def select_blocks(q_pooled, k_pooled, table, frames, tokens_per_frame, cap=None,
-                  block_idx=None, block_cnt=None, want_scores=False, dtype=BF16, stream=None):
-    """Kept key-block lists: ``(block_idx [H, nb, cap], block_cnt [H, nb], scores or None)``."""
+                  block_idx=None, block_cnt=None, want_scores=False, dtype=BF16, workspace=None,
+                  stream=None):
+    """Kept key-block lists: ``(block_idx [H, nb, cap], block_cnt [H, nb], scores or None)``.
+
+    ``workspace``: None for the single-launch path, or a contiguous device
+    tensor (any dtype, 16-byte aligned) for the two-launch path; see
+    ``select_workspace_bytes``."""
     import torch
 
     H, nb, _ = q_pooled.shape
@@ -196,9 +213,11 @@ def select_blocks(q_pooled, k_pooled, table, frames, tokens_per_frame, cap=None,
         block_cnt = torch.empty((H, nb), dtype=torch.int32, device=dev)
     scores = torch.zeros((H, nb, nb), dtype=torch.float64, device=dev) if want_scores else None
     p = problem(H, frames, tokens_per_frame, dtype)
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _check(_lib().saf3r_select_blocks(ctypes.byref(p), head_table(table), _ptr(q_pooled),
                                       _ptr(k_pooled), _ptr(block_idx), _ptr(block_cnt), int(cap),
-                                      _ptr(scores), _stream(stream)),
+                                      _ptr(scores), _ptr(workspace), ctypes.c_int64(ws_bytes),
+                                      _stream(stream)),
            "saf3r_select_blocks")
     return block_idx, block_cnt, scores
 

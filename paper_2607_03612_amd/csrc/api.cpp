@@ -166,10 +166,22 @@ saf3r_status saf3r_estimate_blocks(const saf3r_problem* problem, const saf3r_hea
                                        static_cast<hipStream_t>(stream)));
 }
 
+int64_t saf3r_select_workspace_bytes(const saf3r_problem* problem, const saf3r_head_cfg* table) {
+  Shape s;
+  saf3r_status st = check_problem(problem, &s);
+  if (st != SAF3R_OK) return st;
+  st = check_table(s, table);
+  if (st != SAF3R_OK) return st;
+  int64_t topk_heads = 0;
+  for (int h = 0; h < s.heads; ++h) topk_heads += table[h].pattern == SAF3R_TOPK ? 1 : 0;
+  return topk_heads * s.nb * (int64_t)saf3r::topk_ws_row_bytes(s.nb);
+}
+
 saf3r_status saf3r_select_blocks(const saf3r_problem* problem, const saf3r_head_cfg* table,
                                  const double* q_pooled, const double* k_pooled,
                                  int32_t* block_idx, int32_t* block_cnt, int32_t cap,
-                                 double* scores_or_null, void* stream) {
+                                 double* scores_or_null, void* workspace_or_null,
+                                 int64_t workspace_bytes, void* stream) {
   Shape s;
   saf3r_status st = check_problem(problem, &s);
   if (st != SAF3R_OK) return st;
@@ -206,23 +218,45 @@ saf3r_status saf3r_select_blocks(const saf3r_problem* problem, const saf3r_head_
       sa.param[sa.n_heads++] = table[h].param;
     }
   }
-  // Query blocks scored per workgroup: the most (up to 16) whose score rows
-  // fit in LDS; each key-block read is then shared by that many rows.
+  // Without a workspace: query blocks scored per workgroup, the most (up to
+  // 16) whose score rows fit in LDS; each key-block read is then shared by
+  // that many rows. With one: as many Top-K heads per pair of launches as
+  // the workspace holds.
   constexpr size_t kLdsBudget = 150 * 1024;
   int rows = 16;
   while (rows > 1 && saf3r::topk_lds_bytes(rows, s.nb) > kLdsBudget) rows /= 2;
   ta.rows_per_group = rows;
   const size_t lds = saf3r::topk_lds_bytes(rows, s.nb);
-  if (lds > kLdsBudget) return SAF3R_ERR_UNSUPPORTED;
+  const int64_t head_bytes = (int64_t)s.nb * (int64_t)saf3r::topk_ws_row_bytes(s.nb);
+  int batch = ta.n_heads;
+  if (workspace_or_null) {
+    if (workspace_bytes < 0) return SAF3R_ERR_INVALID_ARGUMENT;
+    if (ta.n_heads > 0 && workspace_bytes < head_bytes) return SAF3R_ERR_CAPACITY;
+    if (ta.n_heads > 0) batch = (int)std::min<int64_t>(ta.n_heads, workspace_bytes / head_bytes);
+  } else if (lds > kLdsBudget) {
+    return SAF3R_ERR_UNSUPPORTED;
+  }
 
   hipStream_t hs = static_cast<hipStream_t>(stream);
   hipError_t e = saf3r::launch_select_static(block_idx, block_cnt, sa, hs);
   if (e != hipSuccess) return SAF3R_ERR_HIP;
   e = saf3r::launch_select_global(q_pooled, k_pooled, block_idx, block_cnt, scores_or_null, ga, hs);
   if (e != hipSuccess) return SAF3R_ERR_HIP;
-  e = saf3r::launch_select_topk(q_pooled, k_pooled, block_idx, block_cnt, scores_or_null, ta,
-                                lds, hs);
-  return hip_status(e);
+  if (!workspace_or_null)
+    return hip_status(saf3r::launch_select_topk(q_pooled, k_pooled, block_idx, block_cnt,
+                                                scores_or_null, ta, lds, hs));
+  for (int b0 = 0; b0 < ta.n_heads; b0 += batch) {
+    saf3r::TopKArgs tb = ta;
+    tb.n_heads = std::min(batch, ta.n_heads - b0);
+    for (int q = 0; q < tb.n_heads; ++q) {
+      tb.head[q] = ta.head[b0 + q];
+      tb.topk[q] = ta.topk[b0 + q];
+    }
+    e = saf3r::launch_select_topk_ws(q_pooled, k_pooled, static_cast<uint32_t*>(workspace_or_null),
+                                     block_idx, block_cnt, scores_or_null, tb, hs);
+    if (e != hipSuccess) return SAF3R_ERR_HIP;
+  }
+  return SAF3R_OK;
 }
 
 saf3r_status saf3r_sparse_attention(const saf3r_problem* problem, const saf3r_head_cfg* table,

@@ -108,6 +108,11 @@ hipError_t launch_attention(int dtype, const void* q, const void* k, const void*
 
 // Bytes of LDS the Top-K selection kernel needs for `rows` query blocks.
 size_t topk_lds_bytes(int rows, int nb);
+// workspace path of the Top-K selection: bytes of one query block's key row,
+// and the two launches (scores into `keys`, then one wave per row)
+size_t topk_ws_row_bytes(int nb);
+hipError_t launch_select_topk_ws(const double* qp, const double* kpT, uint32_t* keys, int32_t* idx,
+                                 int32_t* cnt, double* scores, const TopKArgs& a, hipStream_t s);
 // Threads per workgroup of the Top-K selection kernel for `rows` query blocks.
 int topk_threads(int rows);
 

@@ -37,6 +37,8 @@
 // by an 8-bit-digit radix select over the 64-bit keys, writes the kept
 // blocks ascending (keys equal to the k-th go to the lowest indices), and a
 // second launch copies that list to every query block.
+#include <algorithm>
+
 #include "saf3r_internal.h"
 
 namespace saf3r {
@@ -224,6 +226,243 @@ constexpr int kRowPad = 128;
 constexpr int kPackedKeys = 512;
 constexpr int kPivotSlack = 4;
 
+// The kept blocks of one query block (row r of the 16-row group at i0) from
+// its high keys in `row`. `lrow` is LDS scratch of 64 * row_chunk(nb)
+// words, free to overwrite (the keys are in registers, or for MAXK = 0 are
+// the row itself, whose bucket slots stage 2 overwrites with low halves).
+// Writes the ascending list to dst[0, cap) (padded with -1) and the count to
+// *cnt_row.
+template <int MAXK>
+__device__ inline void select_row(RowKeys<MAXK>& row, uint32_t* lrow, int32_t* dst,
+                                  int32_t* cnt_row, const double* qp_head, const double* kT,
+                                  int i0, int r, int k, int nb, int cap, int lane) {
+  constexpr int kMaskWords = MAXK > 0 ? 1 : 4;  // C <= 48, or <= 256 (nb <= 16384)
+  const int C = row.C;
+
+  // Kept: hi > T, plus `need` of the hi == T bucket (the best by stage 2),
+  // or every hi >= T when a threshold splits off exactly k keys.
+  uint32_t T = 1;
+  bool take_ge = true;
+  int need = 0;
+  uint32_t T2 = 0;
+  int need2 = 0;
+  uint64_t memb[kMaskWords];  // bit e of word e/64: slot e of this lane is in the bucket
+#pragma unroll
+  for (int w = 0; w < kMaskWords; ++w) memb[w] = 0;
+  if (k < nb) {
+    // bracket: count(>= lo) > k > count(>= hi); thresholds are 33-bit so
+    // that hi = 2^32 (counted by nobody) fits
+    uint64_t lo = 1, hi = 1ull << 32;
+    int c_lo = nb, c_hi = 0;
+    bool exact = false;
+    if constexpr (MAXK > 8) {
+      if (C >= 8) {
+        // pivots from the sample of keys l*C (made distinct by the lane
+        // in the low 6 bits): ranks about kPivotSlack samples on either
+        // side of the expected rank k*64/nb of the k-th key
+        const uint32_t xs = (row.r[0] & 0xffffffc0u) | (uint32_t)lane;
+        wave_lds_handover();
+        lrow[lane] = xs;  // the row is in registers; its LDS is scratch now
+        wave_lds_handover();
+        int g = 0;
+#pragma unroll
+        for (int s2 = 0; s2 < 64; ++s2) g += lrow[s2] > xs ? 1 : 0;
+        const int64_t k64 = (int64_t)k * 64;
+        const int rank_hi = k64 >= (int64_t)kPivotSlack * nb
+                                ? (int)((k64 - (int64_t)kPivotSlack * nb) / nb) : -1;
+        const int rank_lo = (int)((k64 + (int64_t)kPivotSlack * nb + nb - 1) / nb);
+        uint64_t p_lo = 1, p_hi = 1ull << 32;
+        if (rank_hi >= 0)
+          p_hi = (uint64_t)(uint32_t)__builtin_amdgcn_readlane(
+                     (int)xs, __builtin_ctzll(__ballot(g == rank_hi))) + 1;
+        if (rank_lo <= 63)
+          p_lo = max((uint32_t)__builtin_amdgcn_readlane(
+                         (int)xs, __builtin_ctzll(__ballot(g == rank_lo))) & 0xffffffc0u, 1u);
+        // one pass counts both pivots (count(>= p_lo) in the low half)
+        const bool hi_inf = p_hi >> 32;
+        const uint32_t t_lo = (uint32_t)p_lo, t_hi = (uint32_t)p_hi;
+        uint32_t pc = 0;
+        row.each([&](int, uint32_t x) {
+          pc += (x >= t_lo ? 1u : 0u) + (!hi_inf && x >= t_hi ? 0x10000u : 0u);
+        });
+        const uint32_t tot = wave_total(pc);
+        const int cl = (int)(tot & 0xffffu), ch = (int)(tot >> 16);
+        if (cl == k) {
+          exact = true;
+          T = t_lo;
+        } else if (!hi_inf && ch == k) {
+          exact = true;
+          T = t_hi;
+        } else {
+          if (ch > k) {
+            lo = p_hi;
+            c_lo = ch;
+          } else if (cl > k) {
+            lo = p_lo;
+            c_lo = cl;
+          }
+          if (cl < k) {
+            hi = p_lo;
+            c_hi = cl;
+          } else if (ch < k) {
+            hi = p_hi;
+            c_hi = ch;
+          }
+        }
+      }
+    }
+    bool packed = false;
+    int c_above = 0;  // keys at or above the packed bracket's top
+    uint32_t pk[kPackedKeys / 64];
+#pragma unroll
+    for (int q = 0; q < kPackedKeys / 64; ++q) pk[q] = 0u;
+    while (!exact && hi - lo > 1) {
+      if constexpr (MAXK > 8) {
+        // pack the bracket's keys into LDS slots [0, c_lo - c_hi); keys
+        // outside it go to a per-lane dummy slot at the row's end
+        if (!packed && C >= 10 && c_lo - c_hi <= kPackedKeys) {
+          const uint32_t lo32 = (uint32_t)lo, span = (uint32_t)(hi - lo - 1);
+          uint32_t n = 0;
+          row.each([&](int, uint32_t x) { n += x - lo32 <= span ? 1u : 0u; });
+          uint32_t pos = wave_scan_incl(n) - n;
+          const uint32_t dummy = (uint32_t)(nb - 64 + lane);
+          wave_lds_handover();
+          row.each([&](int, uint32_t x) {
+            const bool in = x - lo32 <= span;
+            lrow[in ? pos : dummy] = x;
+            pos += in ? 1u : 0u;
+          });
+          wave_lds_handover();
+          const int ncand = c_lo - c_hi;
+#pragma unroll
+          for (int q = 0; q < kPackedKeys / 64; ++q)
+            pk[q] = 64 * q + lane < ncand ? lrow[64 * q + lane] : 0u;
+          c_above = c_hi;
+          packed = true;
+        }
+      }
+      const uint64_t mid = lo + (hi - lo) / 2;
+      const uint32_t t = (uint32_t)mid;
+      int c;
+      if (packed) {
+        uint32_t n = 0;
+#pragma unroll
+        for (int q = 0; q < kPackedKeys / 64; ++q) n += pk[q] >= t ? 1u : 0u;
+        c = c_above + (int)wave_total(n);
+      } else {
+        c = (int)wave_total(row.lane_count_ge(t));
+      }
+      if (c == k) {
+        exact = true;
+        T = t;
+      } else if (c > k) {
+        lo = mid;
+        c_lo = c;
+      } else {
+        hi = mid;
+        c_hi = c;
+      }
+    }
+    if (!exact) {
+      // hi == lo + 1: the bucket of high key T holds c_lo - c_hi > need
+      // keys. Stage 2: exact low halves of its members from their
+      // recomputed score tiles, written over the members' LDS slots.
+      take_ge = false;
+      T = (uint32_t)lo;
+      need = k - c_hi;
+      row.each([&](int e, uint32_t x) {
+        if (x == T) memb[e >> 6] |= 1ull << (e & 63);
+      });
+      const QOperand qa = load_q_operand(qp_head, i0, nb, lane);
+      uint32_t lmn = 0xffffffffu, lmx = 0u;
+      wave_lds_handover();
+      for (int e = 0; e < C; ++e) {
+        uint64_t members = __ballot((memb[e >> 6] >> (e & 63)) & 1);
+        while (members) {
+          const int b = __ffsll((unsigned long long)members) - 1;
+          members &= members - 1;
+          const int j = b * C + e;
+          const f64x4 t = score_tile(qa, load_k_column(kT, nb, j >> 4, lane));
+          const double v = __shfl(t[r >> 2], (j & 15) + 16 * (r & 3));
+          const uint32_t lo_key = (uint32_t)order_key(v * 0.125);
+          if (lane == 0) lrow[j] = lo_key;
+          lmn = min(lmn, lo_key);
+          lmx = max(lmx, lo_key);
+        }
+      }
+      wave_lds_handover();
+      auto count_lo = [&](uint32_t t) {
+        uint32_t c = 0;
+        for (int e = 0; e < C; ++e) {
+          if ((memb[e >> 6] >> (e & 63)) & 1) c += lrow[min(row.base + e, nb - 1)] >= t ? 1u : 0u;
+        }
+        return (int)wave_total(c);
+      };
+      int gt2;
+      bool exact2;
+      T2 = kth_largest(lmn, lmx, need, count_lo, &gt2, &exact2);
+      need2 = exact2 ? 0 : need - gt2;
+      if (exact2) T2 = T2 - 1;  // members with lo > T2 are exactly the ones needed
+    }
+  }
+
+  // ascending output
+  if (MAXK > 0 && take_ge && k + 64 <= nb) {
+    // every key >= T, k of them: each lane writes its kept indices to LDS
+    // slots [0, k) from its prefix-sum offset (others to a dummy slot among
+    // the row's last 64), then the list goes out coalesced
+    const uint32_t n = row.lane_count_ge(T);
+    uint32_t pos = wave_scan_incl(n) - n;
+    const uint32_t dummy = (uint32_t)(nb - 64 + lane);
+    wave_lds_handover();
+    row.each([&](int e, uint32_t x) {
+      const bool kept = x >= T;
+      lrow[kept ? pos : dummy] = (uint32_t)(row.base + e);
+      pos += kept ? 1u : 0u;
+    });
+    wave_lds_handover();
+    for (int p = lane; p < cap; p += 64) dst[p] = p < k ? (int32_t)lrow[p] : -1;
+    if (lane == 0) *cnt_row = k;
+    return;
+  }
+  // general case: per-lane counts of keys kept outright (low half) and
+  // of tie-set keys (high half), prefix-summed over the wave
+  auto classify = [&](int e, uint32_t key_hi, bool* strict, bool* is_eq) {
+    const bool member = (memb[e >> 6] >> (e & 63)) & 1;
+    if (take_ge) {
+      *strict = key_hi >= T;
+      *is_eq = false;
+    } else {
+      const uint32_t lo_key = member ? lrow[min(row.base + e, nb - 1)] : 0u;
+      *strict = (!member && key_hi > T) || (member && lo_key > T2);
+      *is_eq = member && lo_key == T2;
+    }
+  };
+  uint32_t packed_counts = 0;
+  row.each([&](int e, uint32_t key_hi) {
+    bool strict, is_eq;
+    classify(e, key_hi, &strict, &is_eq);
+    packed_counts += (strict ? 1u : 0u) + (is_eq ? 0x10000u : 0u);
+  });
+  const uint32_t incl = wave_scan_incl(packed_counts);
+  const uint32_t excl = incl - packed_counts;
+  const uint32_t total = (uint32_t)__builtin_amdgcn_readlane((int)incl, 63);
+  const int take = take_ge ? 0 : need2;
+  int eq_before = (int)(excl >> 16);
+  int pos = (int)(excl & 0xffffu) + min(eq_before, take);
+  const int out_total = (int)(total & 0xffffu) + min((int)(total >> 16), take);
+  row.each([&](int e, uint32_t key_hi) {
+    bool strict, is_eq;
+    classify(e, key_hi, &strict, &is_eq);
+    const bool sel = strict || (is_eq && eq_before < take);
+    if (sel && pos < cap) dst[pos] = row.base + e;
+    pos += sel ? 1 : 0;
+    eq_before += is_eq ? 1 : 0;
+  });
+  for (int p = out_total + lane; p < cap; p += 64) dst[p] = -1;
+  if (lane == 0) *cnt_row = out_total;
+}
+
 template <int R, int THREADS, int MAXK>
 __global__ __launch_bounds__(THREADS) void select_topk_kernel(const double* __restrict__ qp,
                                                              const double* __restrict__ kpT,
@@ -272,237 +511,90 @@ __global__ __launch_bounds__(THREADS) void select_topk_kernel(const double* __re
   __syncthreads();
 
   // ---- selection: one wave per query block
-  constexpr int kMaskWords = MAXK > 0 ? 1 : 4;  // C <= 48, or <= 256 (nb <= 16384)
   for (int r = wave; r < rows; r += kWaves) {
     uint32_t* lrow = keys + r * ld;
-    int32_t* dst = idx + ((int64_t)h * nb + i0 + r) * a.cap;
     RowKeys<MAXK> row;
     row.init(lrow, nb, lane);
-    const int C = row.C;
-
-    // Kept: hi > T, plus `need` of the hi == T bucket (the best by stage 2),
-    // or every hi >= T when a threshold splits off exactly k keys.
-    uint32_t T = 1;
-    bool take_ge = true;
-    int need = 0;
-    uint32_t T2 = 0;
-    int need2 = 0;
-    uint64_t memb[kMaskWords];  // bit e of word e/64: slot e of this lane is in the bucket
-#pragma unroll
-    for (int w = 0; w < kMaskWords; ++w) memb[w] = 0;
-    if (k < nb) {
-      // bracket: count(>= lo) > k > count(>= hi); thresholds are 33-bit so
-      // that hi = 2^32 (counted by nobody) fits
-      uint64_t lo = 1, hi = 1ull << 32;
-      int c_lo = nb, c_hi = 0;
-      bool exact = false;
-      if constexpr (MAXK > 8) {
-        if (C >= 8) {
-          // pivots from the sample of keys l*C (made distinct by the lane
-          // in the low 6 bits): ranks about kPivotSlack samples on either
-          // side of the expected rank k*64/nb of the k-th key
-          const uint32_t xs = (row.r[0] & 0xffffffc0u) | (uint32_t)lane;
-          wave_lds_handover();
-          lrow[lane] = xs;  // the row is in registers; its LDS is scratch now
-          wave_lds_handover();
-          int g = 0;
-#pragma unroll
-          for (int s2 = 0; s2 < 64; ++s2) g += lrow[s2] > xs ? 1 : 0;
-          const int64_t k64 = (int64_t)k * 64;
-          const int rank_hi = k64 >= (int64_t)kPivotSlack * nb
-                                  ? (int)((k64 - (int64_t)kPivotSlack * nb) / nb) : -1;
-          const int rank_lo = (int)((k64 + (int64_t)kPivotSlack * nb + nb - 1) / nb);
-          uint64_t p_lo = 1, p_hi = 1ull << 32;
-          if (rank_hi >= 0)
-            p_hi = (uint64_t)(uint32_t)__builtin_amdgcn_readlane(
-                       (int)xs, __builtin_ctzll(__ballot(g == rank_hi))) + 1;
-          if (rank_lo <= 63)
-            p_lo = max((uint32_t)__builtin_amdgcn_readlane(
-                           (int)xs, __builtin_ctzll(__ballot(g == rank_lo))) & 0xffffffc0u, 1u);
-          // one pass counts both pivots (count(>= p_lo) in the low half)
-          const bool hi_inf = p_hi >> 32;
-          const uint32_t t_lo = (uint32_t)p_lo, t_hi = (uint32_t)p_hi;
-          uint32_t pc = 0;
-          row.each([&](int, uint32_t x) {
-            pc += (x >= t_lo ? 1u : 0u) + (!hi_inf && x >= t_hi ? 0x10000u : 0u);
-          });
-          const uint32_t tot = wave_total(pc);
-          const int cl = (int)(tot & 0xffffu), ch = (int)(tot >> 16);
-          if (cl == k) {
-            exact = true;
-            T = t_lo;
-          } else if (!hi_inf && ch == k) {
-            exact = true;
-            T = t_hi;
-          } else {
-            if (ch > k) {
-              lo = p_hi;
-              c_lo = ch;
-            } else if (cl > k) {
-              lo = p_lo;
-              c_lo = cl;
-            }
-            if (cl < k) {
-              hi = p_lo;
-              c_hi = cl;
-            } else if (ch < k) {
-              hi = p_hi;
-              c_hi = ch;
-            }
-          }
-        }
-      }
-      bool packed = false;
-      int c_above = 0;  // keys at or above the packed bracket's top
-      uint32_t pk[kPackedKeys / 64];
-#pragma unroll
-      for (int q = 0; q < kPackedKeys / 64; ++q) pk[q] = 0u;
-      while (!exact && hi - lo > 1) {
-        if constexpr (MAXK > 8) {
-          // pack the bracket's keys into LDS slots [0, c_lo - c_hi); keys
-          // outside it go to a per-lane dummy slot at the row's end
-          if (!packed && C >= 10 && c_lo - c_hi <= kPackedKeys) {
-            const uint32_t lo32 = (uint32_t)lo, span = (uint32_t)(hi - lo - 1);
-            uint32_t n = 0;
-            row.each([&](int, uint32_t x) { n += x - lo32 <= span ? 1u : 0u; });
-            uint32_t pos = wave_scan_incl(n) - n;
-            const uint32_t dummy = (uint32_t)(nb - 64 + lane);
-            wave_lds_handover();
-            row.each([&](int, uint32_t x) {
-              const bool in = x - lo32 <= span;
-              lrow[in ? pos : dummy] = x;
-              pos += in ? 1u : 0u;
-            });
-            wave_lds_handover();
-            const int ncand = c_lo - c_hi;
-#pragma unroll
-            for (int q = 0; q < kPackedKeys / 64; ++q)
-              pk[q] = 64 * q + lane < ncand ? lrow[64 * q + lane] : 0u;
-            c_above = c_hi;
-            packed = true;
-          }
-        }
-        const uint64_t mid = lo + (hi - lo) / 2;
-        const uint32_t t = (uint32_t)mid;
-        int c;
-        if (packed) {
-          uint32_t n = 0;
-#pragma unroll
-          for (int q = 0; q < kPackedKeys / 64; ++q) n += pk[q] >= t ? 1u : 0u;
-          c = c_above + (int)wave_total(n);
-        } else {
-          c = (int)wave_total(row.lane_count_ge(t));
-        }
-        if (c == k) {
-          exact = true;
-          T = t;
-        } else if (c > k) {
-          lo = mid;
-          c_lo = c;
-        } else {
-          hi = mid;
-          c_hi = c;
-        }
-      }
-      if (!exact) {
-        // hi == lo + 1: the bucket of high key T holds c_lo - c_hi > need
-        // keys. Stage 2: exact low halves of its members from their
-        // recomputed score tiles, written over the members' LDS slots.
-        take_ge = false;
-        T = (uint32_t)lo;
-        need = k - c_hi;
-        row.each([&](int e, uint32_t x) {
-          if (x == T) memb[e >> 6] |= 1ull << (e & 63);
-        });
-        const QOperand qa = load_q_operand(qp_head, i0, nb, lane);
-        uint32_t lmn = 0xffffffffu, lmx = 0u;
-        wave_lds_handover();
-        for (int e = 0; e < C; ++e) {
-          uint64_t members = __ballot((memb[e >> 6] >> (e & 63)) & 1);
-          while (members) {
-            const int b = __ffsll((unsigned long long)members) - 1;
-            members &= members - 1;
-            const int j = b * C + e;
-            const f64x4 t = score_tile(qa, load_k_column(kT, nb, j >> 4, lane));
-            const double v = __shfl(t[r >> 2], (j & 15) + 16 * (r & 3));
-            const uint32_t lo_key = (uint32_t)order_key(v * 0.125);
-            if (lane == 0) lrow[j] = lo_key;
-            lmn = min(lmn, lo_key);
-            lmx = max(lmx, lo_key);
-          }
-        }
-        wave_lds_handover();
-        auto count_lo = [&](uint32_t t) {
-          uint32_t c = 0;
-          for (int e = 0; e < C; ++e) {
-            if ((memb[e >> 6] >> (e & 63)) & 1) c += lrow[min(row.base + e, nb - 1)] >= t ? 1u : 0u;
-          }
-          return (int)wave_total(c);
-        };
-        int gt2;
-        bool exact2;
-        T2 = kth_largest(lmn, lmx, need, count_lo, &gt2, &exact2);
-        need2 = exact2 ? 0 : need - gt2;
-        if (exact2) T2 = T2 - 1;  // members with lo > T2 are exactly the ones needed
-      }
-    }
-
-    // ascending output
-    if (MAXK > 0 && take_ge && k + 64 <= nb) {
-      // every key >= T, k of them: each lane writes its kept indices to LDS
-      // slots [0, k) from its prefix-sum offset (others to a dummy slot among
-      // the row's last 64), then the list goes out coalesced
-      const uint32_t n = row.lane_count_ge(T);
-      uint32_t pos = wave_scan_incl(n) - n;
-      const uint32_t dummy = (uint32_t)(nb - 64 + lane);
-      wave_lds_handover();
-      row.each([&](int e, uint32_t x) {
-        const bool kept = x >= T;
-        lrow[kept ? pos : dummy] = (uint32_t)(row.base + e);
-        pos += kept ? 1u : 0u;
-      });
-      wave_lds_handover();
-      for (int p = lane; p < a.cap; p += 64) dst[p] = p < k ? (int32_t)lrow[p] : -1;
-      if (lane == 0) cnt[(int64_t)h * nb + i0 + r] = k;
-      continue;
-    }
-    // general case: per-lane counts of keys kept outright (low half) and
-    // of tie-set keys (high half), prefix-summed over the wave
-    auto classify = [&](int e, uint32_t key_hi, bool* strict, bool* is_eq) {
-      const bool member = (memb[e >> 6] >> (e & 63)) & 1;
-      if (take_ge) {
-        *strict = key_hi >= T;
-        *is_eq = false;
-      } else {
-        const uint32_t lo_key = member ? lrow[min(row.base + e, nb - 1)] : 0u;
-        *strict = (!member && key_hi > T) || (member && lo_key > T2);
-        *is_eq = member && lo_key == T2;
-      }
-    };
-    uint32_t packed_counts = 0;
-    row.each([&](int e, uint32_t key_hi) {
-      bool strict, is_eq;
-      classify(e, key_hi, &strict, &is_eq);
-      packed_counts += (strict ? 1u : 0u) + (is_eq ? 0x10000u : 0u);
-    });
-    const uint32_t incl = wave_scan_incl(packed_counts);
-    const uint32_t excl = incl - packed_counts;
-    const uint32_t total = (uint32_t)__builtin_amdgcn_readlane((int)incl, 63);
-    const int take = take_ge ? 0 : need2;
-    int eq_before = (int)(excl >> 16);
-    int pos = (int)(excl & 0xffffu) + min(eq_before, take);
-    const int out_total = (int)(total & 0xffffu) + min((int)(total >> 16), take);
-    row.each([&](int e, uint32_t key_hi) {
-      bool strict, is_eq;
-      classify(e, key_hi, &strict, &is_eq);
-      const bool sel = strict || (is_eq && eq_before < take);
-      if (sel && pos < a.cap) dst[pos] = row.base + e;
-      pos += sel ? 1 : 0;
-      eq_before += is_eq ? 1 : 0;
-    });
-    for (int p = out_total + lane; p < a.cap; p += 64) dst[p] = -1;
-    if (lane == 0) cnt[(int64_t)h * nb + i0 + r] = out_total;
+    select_row<MAXK>(row, lrow, idx + ((int64_t)h * nb + i0 + r) * a.cap,
+                     cnt + (int64_t)h * nb + i0 + r, qp_head, kT, i0, r, k, nb, a.cap, lane);
   }
+}
+
+// Top-K heads with a workspace: the same scores and the same selection in two
+// launches, so that neither phase leaves the other's units idle on a CU.
+//   1. topk_score_kernel: eight waves score 16 query blocks of one head
+//      (the tiles of select_topk_kernel) and store the high keys as rows of
+//      64 * row_chunk(nb) words in the workspace;
+//   2. topk_rows_kernel: one wave per query block loads its row of keys
+//      (into registers, or into its own LDS row when C > MAXK) and runs
+//      select_row; with little LDS per wave, many rows are in flight per CU.
+constexpr int kScoreWaves = 8;
+
+__global__ __launch_bounds__(kScoreWaves * 64) void topk_score_kernel(
+    const double* __restrict__ qp, const double* __restrict__ kpT, uint32_t* __restrict__ keys,
+    double* __restrict__ scores, TopKArgs a) {
+  const int nb = a.nb;
+  const int groups = (nb + 15) / 16;
+  const int slot = blockIdx.x / groups;
+  const int i0 = (blockIdx.x - slot * groups) * 16;
+  const int rows = min(16, nb - i0);
+  const int h = a.head[slot];
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int64_t ld = 64 * row_chunk(nb);
+  const double* kT = kpT + (int64_t)h * kHeadDim * nb;
+  const double* qp_head = qp + (int64_t)h * nb * kHeadDim;
+  uint32_t* ws = keys + ((int64_t)slot * nb + i0) * ld;
+  const int chunks16 = (nb + 15) / 16;
+  const QOperand qa = load_q_operand(qp_head, i0, nb, lane);
+  KColumn next = load_k_column(kT, nb, min(wave, chunks16 - 1), lane);
+  for (int c = wave; c < chunks16; c += kScoreWaves) {
+    const KColumn cur = next;
+    next = load_k_column(kT, nb, min(c + kScoreWaves, chunks16 - 1), lane);  // prefetch
+    const f64x4 t = score_tile(qa, cur);
+    const int j = 16 * c + (lane & 15);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int r = (lane >> 4) + 4 * e;
+      if (r < rows && j < nb) {
+        const double s = t[e] * 0.125;  // 1/sqrt(64), exact
+        ws[r * ld + j] = (uint32_t)(order_key(s) >> 32);
+        if (scores) scores[((int64_t)h * nb + i0 + r) * nb + j] = s;
+      }
+    }
+  }
+}
+
+template <int MAXK>
+__global__ __launch_bounds__(256) void topk_rows_kernel(const double* __restrict__ qp,
+                                                       const double* __restrict__ kpT,
+                                                       const uint32_t* __restrict__ keys,
+                                                       int32_t* __restrict__ idx,
+                                                       int32_t* __restrict__ cnt, TopKArgs a) {
+  extern __shared__ __attribute__((aligned(16))) uint32_t srow[];  // [waves][ld]
+  const int nb = a.nb;
+  const int lane = threadIdx.x & 63;
+  const int wl = threadIdx.x >> 6;
+  const int64_t w = (int64_t)blockIdx.x * (blockDim.x >> 6) + wl;
+  if (w >= (int64_t)a.n_heads * nb) return;  // whole waves; no barrier below
+  const int slot = (int)(w / nb);
+  const int i = (int)(w - (int64_t)slot * nb);
+  const int h = a.head[slot];
+  const int64_t ld = 64 * row_chunk(nb);
+  uint32_t* lrow = srow + wl * ld;
+  const uint32_t* grow = keys + ((int64_t)slot * nb + i) * ld;
+  RowKeys<MAXK> row;
+  if constexpr (MAXK > 0) {
+    row.init(grow, nb, lane);
+  } else {
+    for (int64_t q = lane; q < ld / 4; q += 64)
+      reinterpret_cast<u32x4*>(lrow)[q] = reinterpret_cast<const u32x4*>(grow)[q];
+    wave_lds_handover();
+    row.init(lrow, nb, lane);
+  }
+  select_row<MAXK>(row, lrow, idx + ((int64_t)h * nb + i) * a.cap, cnt + (int64_t)h * nb + i,
+                   qp + (int64_t)h * nb * kHeadDim, kpT + (int64_t)h * kHeadDim * nb, i & ~15,
+                   i & 15, a.topk[slot], nb, a.cap, lane);
 }
 
 // One wave per (head, query block) of the static-pattern heads (DENSE,
@@ -748,6 +840,36 @@ hipError_t launch_select_topk(const double* qp, const double* kpT, int32_t* idx,
     case 1: return launch_topk_rows<1, 256>(qp, kpT, idx, cnt, scores, a, lds, s);
     default: return hipErrorInvalidValue;
   }
+}
+
+size_t topk_ws_row_bytes(int nb) { return (size_t)64 * row_chunk(nb) * sizeof(uint32_t); }
+
+hipError_t launch_select_topk_ws(const double* qp, const double* kpT, uint32_t* keys, int32_t* idx,
+                                 int32_t* cnt, double* scores, const TopKArgs& a, hipStream_t s) {
+  if (a.n_heads == 0) return hipSuccess;
+  const int groups = (a.nb + 15) / 16;
+  hipLaunchKernelGGL(topk_score_kernel, dim3((unsigned)(groups * a.n_heads)),
+                     dim3(kScoreWaves * 64), 0, s, qp, kpT, keys, scores, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  // waves per workgroup: as many rows as fit in 64 KB of LDS, at most four
+  const size_t row_bytes = topk_ws_row_bytes(a.nb);
+  const int wpg = (int)std::max<size_t>(1, std::min<size_t>(4, (64 * 1024) / row_bytes));
+  const size_t lds = (size_t)wpg * row_bytes;
+  const int64_t waves = (int64_t)a.n_heads * a.nb;
+  const dim3 grid((unsigned)((waves + wpg - 1) / wpg)), block(64 * wpg);
+  auto go = [&](auto kern) -> hipError_t {
+    hipError_t e2 = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e2 != hipSuccess) return e2;
+    hipLaunchKernelGGL(kern, grid, block, lds, s, qp, kpT, keys, idx, cnt, a);
+    return hipGetLastError();
+  };
+  const int chunks = row_chunk(a.nb);
+  if (chunks <= 4) return go(topk_rows_kernel<4>);
+  if (chunks <= 16) return go(topk_rows_kernel<16>);
+  if (chunks <= 48) return go(topk_rows_kernel<48>);
+  return go(topk_rows_kernel<0>);
 }
 
 hipError_t launch_select_global(const double* qp, const double* kpT, int32_t* idx, int32_t* cnt,

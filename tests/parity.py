@@ -31,15 +31,30 @@ def out_to_numpy(t):
         t.cpu().numpy().astype(np.float64)
 
 
-def gpu_layer(P, w, q, k, v, table, want_scores=False, want_lse=True):
-    """Runs estimate -> select -> attend through the binding; returns numpy results."""
+def select_workspace(P, table, w, heads=None):
+    """A device workspace for the two-launch Top-K selection: the full size,
+    or the share of `heads` TOPK heads."""
+    import torch
+
+    code = P.BF16 if w.dtype == "bf16" else P.F32
+    full = P.select_workspace_bytes(table, w.frames, w.tokens_per_frame, code)
+    n_topk = sum(1 for p, _ in table if p == 2)
+    nbytes = full if heads is None or n_topk == 0 else full // n_topk * heads
+    return torch.empty(max(nbytes, 16) // 4, dtype=torch.int32, device="cuda")
+
+
+def gpu_layer(P, w, q, k, v, table, want_scores=False, want_lse=True, workspace=True):
+    """Runs estimate -> select -> attend through the binding; returns numpy
+    results. `workspace`: the two-launch Top-K selection (as bench.py runs
+    it) or, when False, the single-launch one."""
     import torch
 
     tq, tk, tv = (to_device(x, w.dtype) for x in (q, k, v))
     qp, kp = P.estimate_blocks(tq, tk, table, w.frames, w.tokens_per_frame)
     code = P.BF16 if w.dtype == "bf16" else P.F32
+    ws = select_workspace(P, table, w) if workspace else None
     idx, cnt, scores = P.select_blocks(qp, kp, table, w.frames, w.tokens_per_frame,
-                                       want_scores=want_scores, dtype=code)
+                                       want_scores=want_scores, dtype=code, workspace=ws)
     out, lse = P.sparse_attention(tq, tk, tv, table, w.frames, w.tokens_per_frame, idx, cnt,
                                   want_lse=want_lse)
     torch.cuda.synchronize()

@@ -114,10 +114,18 @@ def test_calls_reject_bad_arguments_before_launch(B):
     fake = ctypes.c_void_p(0x1000)  # never dereferenced: validation fails first
     assert lib.saf3r_estimate_blocks(ctypes.byref(p), t, None, fake, fake, fake, None) == -1
     assert lib.saf3r_estimate_blocks(ctypes.byref(_p(B, head_dim=32)), t, fake, fake, fake, fake, None) == -2
-    assert lib.saf3r_select_blocks(ctypes.byref(p), t, fake, fake, fake, fake, 3, None, None) == -3
-    assert lib.saf3r_select_blocks(ctypes.byref(p), t, fake, None, fake, fake, 8, None, None) == -1
-    assert lib.saf3r_select_blocks(ctypes.byref(p), B.head_table([(1, 0), (2, 9)]),
-                                   fake, fake, fake, fake, 8, None, None) == -5
+    sel = lib.saf3r_select_blocks
+    assert sel(ctypes.byref(p), t, fake, fake, fake, fake, 3, None, None, 0, None) == -3
+    assert sel(ctypes.byref(p), t, fake, None, fake, fake, 8, None, None, 0, None) == -1
+    assert sel(ctypes.byref(p), B.head_table([(1, 0), (2, 9)]),
+               fake, fake, fake, fake, 8, None, None, 0, None) == -5
+    # workspace: one TOPK head of nb = 4 blocks takes 4 rows of 64 x 4 words
+    need = lib.saf3r_select_workspace_bytes(ctypes.byref(p), t)
+    assert need == 4 * 64 * 4 * 4
+    assert lib.saf3r_select_workspace_bytes(ctypes.byref(p), B.head_table([(1, 0), (0, 0)])) == 0
+    assert lib.saf3r_select_workspace_bytes(None, t) == -1
+    assert sel(ctypes.byref(p), t, fake, fake, fake, fake, 8, None, fake, need - 16, None) == -3
+    assert sel(ctypes.byref(p), t, fake, fake, fake, fake, 8, None, fake, -1, None) == -1
     assert lib.saf3r_sparse_attention(ctypes.byref(p), t, fake, fake, fake, fake, fake, 4,
                                       None, None, None) == -1
     assert lib.saf3r_sparse_attention(ctypes.byref(p), t, fake, fake, fake, None, fake, 4,

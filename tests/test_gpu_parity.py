@@ -123,6 +123,42 @@ def test_maximum_size_sampled(gpu_lib):
     _sampled_check(P, w, 0, samples=6, seed=11)
 
 
+@pytest.mark.parametrize("name,layer", [("S4xT261-f32", 0), ("S8xT1374-bf16", 0),
+                                        ("S32xT1374-bf16", 0), ("S100xT1374-bf16", 0),
+                                        ("S200xT1374-bf16-L24", 3)])
+def test_select_paths_agree(gpu_lib, name, layer):
+    """The single-launch Top-K selection (score rows in LDS) and the
+    two-launch one (scores in a workspace, one wave per row), with a full
+    workspace and with room for one head only (heads in batches), give the
+    same lists, counts and scores bit for bit. S200 (nb = 4294) takes the
+    row-in-LDS variant of the second launch."""
+    import torch
+
+    import paper_2607_03612_amd as P
+
+    w = WORKLOADS[name]
+    q, k, _ = make_qkv(w, layer=layer)
+    table = make_table(w, layer=layer)
+    code = P.BF16 if w.dtype == "bf16" else P.F32
+    tq, tk = (PT.to_device(x, w.dtype) for x in (q, k))
+    qp, kp = P.estimate_blocks(tq, tk, table, w.frames, w.tokens_per_frame)
+    small = w.nb <= 1024  # the full score matrix is only kept for small layers
+    runs = []
+    for ws in (None, PT.select_workspace(P, table, w), PT.select_workspace(P, table, w, heads=1)):
+        cap = P.index_capacity(table, w.frames, w.tokens_per_frame, code)
+        idx = torch.full((w.heads, w.nb, cap), -7, dtype=torch.int32, device="cuda")
+        cnt = torch.full((w.heads, w.nb), -9, dtype=torch.int32, device="cuda")
+        _, _, sc = P.select_blocks(qp, kp, table, w.frames, w.tokens_per_frame, cap, idx, cnt,
+                                   want_scores=small, dtype=code, workspace=ws)
+        torch.cuda.synchronize()
+        runs.append((idx.cpu().numpy(), cnt.cpu().numpy(), None if sc is None else sc.cpu().numpy()))
+    for idx, cnt, sc in runs[1:]:
+        assert np.array_equal(cnt, runs[0][1])
+        assert np.array_equal(idx, runs[0][0])
+        if small:
+            assert np.array_equal(sc.view(np.uint64), runs[0][2].view(np.uint64))
+
+
 # ------------------------------------------------------------ edge cases
 
 EDGE = [
