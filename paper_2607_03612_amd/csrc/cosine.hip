@@ -18,6 +18,8 @@
 //      a prefix sum over the frames, into every head that keeps k per frame.
 // The lists depend on the features only, so they are computed once per
 // sequence and reused by every layer.
+#include <algorithm>
+
 #include "saf3r_internal.h"
 
 namespace saf3r {
@@ -178,18 +180,40 @@ __device__ inline int lane_scan_incl(int v) {
 // of the per-frame kept counts gives the frame's offset in the row, and the
 // lane writes the frame's kept blocks there in ascending order, into the row
 // of every head of the group.
+// kLds: the wave first copies its similarity row into its own LDS row
+// (coalesced), and the lanes' frame scans read LDS instead of scattered
+// global words (rows up to kTopkLdsRow doubles). The row's list is built in
+// the wave's LDS list (cap entries) and then copied, coalesced, into the row
+// of every head of the group.
+constexpr int kTopkLdsRow = 8192;
+
+// list entries kept in LDS: a row keeps at most nb blocks
+__host__ __device__ inline int topk_list_len(const CosineArgs& a) { return a.cap < a.nb ? a.cap : a.nb; }
+
+template <bool kLds>
 __global__ __launch_bounds__(256) void cosine_topk_kernel(const double* __restrict__ sim,
                                                          int32_t* __restrict__ idx,
                                                          int32_t* __restrict__ cnt,
                                                          CosineArgs a) {
+  extern __shared__ double srow[];  // [waves][nb] doubles when kLds, then [waves][cap] ints
   const int lane = threadIdx.x & 63;
-  const int64_t wave = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (wave >= (int64_t)a.n_groups * a.nb) return;
+  const int wl = threadIdx.x >> 6;
+  const int wpg = blockDim.x >> 6;
+  const int64_t wave = (int64_t)blockIdx.x * wpg + wl;
+  if (wave >= (int64_t)a.n_groups * a.nb) return;  // whole waves; no barrier below
   const int g = (int)(wave / a.nb);
   const int i = (int)(wave - (int64_t)g * a.nb);
   const int k = a.group_k[g];
   const int q0 = a.group_start[g], q1 = a.group_start[g + 1];
-  const double* row = sim + (int64_t)i * a.nb;
+  const double* grow = sim + (int64_t)i * a.nb;
+  double* lrow = srow + (int64_t)wl * a.nb;
+  const int list_len = topk_list_len(a);
+  int* llist = reinterpret_cast<int*>(srow + (kLds ? (int64_t)wpg * a.nb : 0)) + (int64_t)wl * list_len;
+  if constexpr (kLds) {
+    for (int j = lane; j < a.nb; j += 64) lrow[j] = grow[j];
+    asm volatile("" ::: "memory");  // a wave's LDS accesses run in order
+  }
+  const double* row = kLds ? lrow : grow;
   const int64_t T = a.tokens_per_frame;
   const int frames = (int)((a.n + T - 1) / T);
   int base = 0;
@@ -227,17 +251,17 @@ __global__ __launch_bounds__(256) void cosine_topk_kernel(const double* __restri
     if (kept > 0) {
       for (int j = j_lo; j < j_hi; ++j) {
         if (ranks_before(tv, tj, row[j], j)) continue;
-        if (pos < a.cap)
-          for (int q = q0; q < q1; ++q) idx[((int64_t)a.head[q] * a.nb + i) * a.cap + pos] = j;
+        if (pos < list_len) llist[pos] = j;
         ++pos;
       }
     }
     base += __shfl(incl, 63);
   }
+  asm volatile("" ::: "memory");  // the list's LDS writes, then the wave's reads
   for (int q = q0; q < q1; ++q) {
     const int h = a.head[q];
     int32_t* dst = idx + ((int64_t)h * a.nb + i) * a.cap;
-    for (int p = base + lane; p < a.cap; p += 64) dst[p] = -1;
+    for (int p = lane; p < a.cap; p += 64) dst[p] = p < base ? llist[p] : -1;
     if (lane == 0) cnt[(int64_t)h * a.nb + i] = base;
   }
 }
@@ -270,9 +294,22 @@ hipError_t launch_cosine(int dtype, const void* f, double* fb, double* sim, int3
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int64_t waves = (int64_t)a.n_groups * a.nb;
-  hipLaunchKernelGGL(cosine_topk_kernel, dim3((unsigned)((waves + 3) / 4)), dim3(256), 0, s, sim,
-                     idx, cnt, a);
-  return hipGetLastError();
+  // per wave: the similarity row (kLds) and the list; waves per workgroup
+  // such that a workgroup takes at most 96 KB of LDS, at most four
+  const bool lds_row = a.nb <= kTopkLdsRow;
+  const size_t wave_bytes = (lds_row ? (size_t)a.nb * sizeof(double) : 0) +
+                            (size_t)topk_list_len(a) * sizeof(int);
+  const int wpg = (int)std::max<size_t>(1, std::min<size_t>(4, (96 * 1024) / wave_bytes));
+  const size_t lds = (size_t)wpg * wave_bytes;
+  const dim3 tgrid((unsigned)((waves + wpg - 1) / wpg)), tblock(64 * wpg);
+  auto go = [&](auto kern) -> hipError_t {
+    hipError_t e2 = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e2 != hipSuccess) return e2;
+    hipLaunchKernelGGL(kern, tgrid, tblock, lds, s, sim, idx, cnt, a);
+    return hipGetLastError();
+  };
+  return lds_row ? go(cosine_topk_kernel<true>) : go(cosine_topk_kernel<false>);
 }
 
 }  // namespace saf3r
