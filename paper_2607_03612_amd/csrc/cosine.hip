@@ -21,6 +21,9 @@
 #include <algorithm>
 
 #include "saf3r_internal.h"
+#ifndef COSINE_SIM_KERNEL
+#define COSINE_SIM_KERNEL cosine_sim_mfma_kernel
+#endif
 
 namespace saf3r {
 namespace {
@@ -159,6 +162,79 @@ __global__ __launch_bounds__(256) void cosine_sim_kernel(const double* __restric
   }
 }
 
+typedef double f64x4 __attribute__((ext_vector_type(4)));
+
+// The same product on the fp64 matrix cores: a 64x64 tile per workgroup,
+// a 32x32 quarter per wave as 2x2 tiles of v_mfma_f64_16x16x4f64 (A: 16 row
+// blocks x 4 dimensions, one double per lane; B: 4 dimensions x 16 column
+// blocks; both read 16 consecutive blocks of one dimension, 128 B). Upper
+// tiles only, mirrored as above.
+__global__ __launch_bounds__(256) void cosine_sim_mfma_kernel(const double* __restrict__ fb,
+                                                             double* __restrict__ sim,
+                                                             CosineArgs a) {
+  const int tiles = (a.nb + 63) / 64;
+  const int ti = blockIdx.x / tiles, tj = blockIdx.x - (blockIdx.x / tiles) * tiles;
+  if (ti > tj) return;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r0 = ti * 64 + 32 * (wave >> 1), c0 = tj * 64 + 32 * (wave & 1);
+  const int nb = a.nb;
+  const int sub = lane >> 4;  // dimension within a group of 4
+  auto operand = [&](int d0, int blk) -> double {
+    const int d = d0 + sub;
+    return d < a.dim && blk < nb ? fb[(int64_t)d * nb + blk] : 0.0;
+  };
+  f64x4 acc[2][2];
+#pragma unroll
+  for (int x = 0; x < 2; ++x)
+#pragma unroll
+    for (int y = 0; y < 2; ++y) acc[x][y] = f64x4{0.0, 0.0, 0.0, 0.0};
+  // 16 dimensions per step (four MFMA groups), the next 16 loading meanwhile
+  constexpr int kSteps = 4;
+  double an[kSteps][2], bn[kSteps][2];
+  auto load_step = [&](int d0, double (&ax)[kSteps][2], double (&bx)[kSteps][2]) {
+#pragma unroll
+    for (int u = 0; u < kSteps; ++u)
+#pragma unroll
+      for (int x = 0; x < 2; ++x) {
+        ax[u][x] = operand(d0 + 4 * u, r0 + 16 * x + (lane & 15));
+        bx[u][x] = operand(d0 + 4 * u, c0 + 16 * x + (lane & 15));
+      }
+  };
+  load_step(0, an, bn);
+  for (int d0 = 0; d0 < a.dim; d0 += 4 * kSteps) {
+    double ac[kSteps][2], bc[kSteps][2];
+#pragma unroll
+    for (int u = 0; u < kSteps; ++u)
+#pragma unroll
+      for (int x = 0; x < 2; ++x) {
+        ac[u][x] = an[u][x];
+        bc[u][x] = bn[u][x];
+      }
+    load_step(d0 + 4 * kSteps, an, bn);
+#pragma unroll
+    for (int u = 0; u < kSteps; ++u) {
+      acc[0][0] = __builtin_amdgcn_mfma_f64_16x16x4f64(ac[u][0], bc[u][0], acc[0][0], 0, 0, 0);
+      acc[0][1] = __builtin_amdgcn_mfma_f64_16x16x4f64(ac[u][0], bc[u][1], acc[0][1], 0, 0, 0);
+      acc[1][0] = __builtin_amdgcn_mfma_f64_16x16x4f64(ac[u][1], bc[u][0], acc[1][0], 0, 0, 0);
+      acc[1][1] = __builtin_amdgcn_mfma_f64_16x16x4f64(ac[u][1], bc[u][1], acc[1][1], 0, 0, 0);
+    }
+  }
+  // element e of a lane: row (lane / 16) + 4e, column lane % 16 of the tile
+#pragma unroll
+  for (int x = 0; x < 2; ++x)
+#pragma unroll
+    for (int y = 0; y < 2; ++y)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int i = r0 + 16 * x + sub + 4 * e;
+        const int j = c0 + 16 * y + (lane & 15);
+        if (i < nb && j < nb) {
+          sim[(int64_t)i * nb + j] = acc[x][y][e];
+          if (ti != tj) sim[(int64_t)j * nb + i] = acc[x][y][e];
+        }
+      }
+}
+
 // (value, index) order of the selection: higher value first, then lower index
 __device__ inline bool ranks_before(double v, int j, double w, int k) {
   return v > w || (v == w && j < k);
@@ -290,7 +366,7 @@ hipError_t launch_cosine(int dtype, const void* f, double* fb, double* sim, int3
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int tiles = (a.nb + 63) / 64;
-  hipLaunchKernelGGL(cosine_sim_kernel, dim3((unsigned)(tiles * tiles)), dim3(256), 0, s, fb, sim, a);
+  hipLaunchKernelGGL(COSINE_SIM_KERNEL, dim3((unsigned)(tiles * tiles)), dim3(256), 0, s, fb, sim, a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int64_t waves = (int64_t)a.n_groups * a.nb;
