@@ -8,9 +8,9 @@
 // linearity argument as the query probe. All of it runs in float64:
 //   1. cosine_pool_kernel: one workgroup per block writes the block's mean
 //      unit feature, dimension-major [D][nb];
-//   2. cosine_sim_kernel: the block similarity matrix [nb][nb] as a 64x64
-//      register-tiled product of that matrix with itself (upper tiles only,
-//      mirrored);
+//   2. cosine_sim_mfma_kernel: the block similarity matrix [nb][nb], the
+//      product of that matrix with itself on the fp64 matrix cores (upper
+//      tiles only, mirrored);
 //   3. cosine_topk_kernel: one wave per (per-frame count k, query block), one
 //      lane per frame (a key block counts under the frame of its first
 //      token): k scans find the frame's k-th best (similarity desc, index
@@ -21,9 +21,6 @@
 #include <algorithm>
 
 #include "saf3r_internal.h"
-#ifndef COSINE_SIM_KERNEL
-#define COSINE_SIM_KERNEL cosine_sim_mfma_kernel
-#endif
 
 namespace saf3r {
 namespace {
@@ -106,69 +103,15 @@ __global__ __launch_bounds__(kPoolThreads) void cosine_pool_kernel(const T* __re
   }
 }
 
-// sim[i][j] = sum_d fb[d][i] fb[d][j]: 64x64 tiles, 16x16 threads of 4x4.
-// The matrix is symmetric: only tiles on or above the diagonal are computed,
-// and an off-diagonal tile is also stored transposed (the same fma sequence
-// with the two factors swapped, so the same bits).
-__global__ __launch_bounds__(256) void cosine_sim_kernel(const double* __restrict__ fb,
-                                                        double* __restrict__ sim, CosineArgs a) {
-  __shared__ double as[16][64];
-  __shared__ double bs[16][64];
-  const int tiles = (a.nb + 63) / 64;
-  const int ti = blockIdx.x / tiles, tj = blockIdx.x - (blockIdx.x / tiles) * tiles;
-  if (ti > tj) return;
-  const int i0 = ti * 64, j0 = tj * 64;
-  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
-  double acc[4][4];
-#pragma unroll
-  for (int x = 0; x < 4; ++x)
-#pragma unroll
-    for (int y = 0; y < 4; ++y) acc[x][y] = 0.0;
-  for (int d0 = 0; d0 < a.dim; d0 += 16) {
-    // stage 16 dimensions of the 64 rows and 64 columns
-    for (int e = threadIdx.x; e < 16 * 64; e += 256) {
-      const int dd = e >> 6, c = e & 63;
-      const int d = d0 + dd;
-      as[dd][c] = d < a.dim && i0 + c < a.nb ? fb[(int64_t)d * a.nb + i0 + c] : 0.0;
-      bs[dd][c] = d < a.dim && j0 + c < a.nb ? fb[(int64_t)d * a.nb + j0 + c] : 0.0;
-    }
-    __syncthreads();
-#pragma unroll
-    for (int dd = 0; dd < 16; ++dd) {
-      double av[4], bv[4];
-#pragma unroll
-      for (int x = 0; x < 4; ++x) av[x] = as[dd][4 * ty + x];
-#pragma unroll
-      for (int y = 0; y < 4; ++y) bv[y] = bs[dd][4 * tx + y];
-#pragma unroll
-      for (int x = 0; x < 4; ++x)
-#pragma unroll
-        for (int y = 0; y < 4; ++y) acc[x][y] = fma(av[x], bv[y], acc[x][y]);
-    }
-    __syncthreads();
-  }
-#pragma unroll
-  for (int x = 0; x < 4; ++x) {
-    const int i = i0 + 4 * ty + x;
-    if (i >= a.nb) continue;
-#pragma unroll
-    for (int y = 0; y < 4; ++y) {
-      const int j = j0 + 4 * tx + y;
-      if (j < a.nb) {
-        sim[(int64_t)i * a.nb + j] = acc[x][y];
-        if (ti != tj) sim[(int64_t)j * a.nb + i] = acc[x][y];
-      }
-    }
-  }
-}
-
 typedef double f64x4 __attribute__((ext_vector_type(4)));
 
-// The same product on the fp64 matrix cores: a 64x64 tile per workgroup,
-// a 32x32 quarter per wave as 2x2 tiles of v_mfma_f64_16x16x4f64 (A: 16 row
-// blocks x 4 dimensions, one double per lane; B: 4 dimensions x 16 column
-// blocks; both read 16 consecutive blocks of one dimension, 128 B). Upper
-// tiles only, mirrored as above.
+// sim[i][j] = sum_d fb[d][i] fb[d][j] on the fp64 matrix cores: a 64x64
+// tile per workgroup, a 32x32 quarter per wave as 2x2 tiles of
+// v_mfma_f64_16x16x4f64 (A: 16 row blocks x 4 dimensions, one double per
+// lane; B: 4 dimensions x 16 column blocks; both read 16 consecutive blocks
+// of one dimension, 128 B). The matrix is symmetric: only tiles on or above
+// the diagonal are computed, and an off-diagonal tile is also stored
+// transposed.
 __global__ __launch_bounds__(256) void cosine_sim_mfma_kernel(const double* __restrict__ fb,
                                                              double* __restrict__ sim,
                                                              CosineArgs a) {
@@ -366,7 +309,7 @@ hipError_t launch_cosine(int dtype, const void* f, double* fb, double* sim, int3
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int tiles = (a.nb + 63) / 64;
-  hipLaunchKernelGGL(COSINE_SIM_KERNEL, dim3((unsigned)(tiles * tiles)), dim3(256), 0, s, fb, sim, a);
+  hipLaunchKernelGGL(cosine_sim_mfma_kernel, dim3((unsigned)(tiles * tiles)), dim3(256), 0, s, fb, sim, a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int64_t waves = (int64_t)a.n_groups * a.nb;
