@@ -287,6 +287,22 @@ def test_maximum_head_count_full_parity(gpu_lib):
     print(f"[parity] {w.name}: near-ties {near}", flush=True)
 
 
+@pytest.mark.parametrize("cls", ["topk1", "topk_nb", "frame_local", "dense", "anchor", "stride5",
+                                 "global2"])
+def test_single_head_each_class(gpu_lib, cls):
+    """A one-head layer of each class (grids and head lists of length one),
+    on a ragged bf16 layer (5 frames x 150 tokens, 12 blocks, last one
+    partial), checked in full against the oracle."""
+    import paper_2607_03612_amd as P
+
+    w = Workload(f"one-{cls}", 5, 150, "bf16", ("fixed", 1, 0, 50), heads=1)
+    spec = {"topk1": (O.TOPK, 1), "topk_nb": (O.TOPK, w.nb), "frame_local": (O.FRAME_LOCAL, 0),
+            "dense": (O.DENSE, 0), "anchor": (O.ANCHOR, 2), "stride5": (O.STRIDE, 5),
+            "global2": (O.GLOBAL_PROBE, 2)}[cls]
+    q, k, v = make_qkv(w)
+    _full_check(P, w, q, k, v, [spec])
+
+
 def test_stride_one_equals_dense_bitwise(gpu_lib):
     import paper_2607_03612_amd as P
 
