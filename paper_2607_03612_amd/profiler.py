@@ -96,12 +96,22 @@ def profile_heads(calib, frames: int, tokens_per_frame: int, candidates, sigma: 
                 costs[c] += [attention_cost(pattern, param, N, ih[h], ch[h]) for h in range(H)]
     errors /= len(calib)
     costs /= len(calib)
+    choice = choose(errors, costs)
+    return {"configs": configs, "errors": errors, "costs": costs, "choice": choice,
+            "table": [configs[c] for c in choice]}
+
+
+def choose(errors, costs) -> list:
+    """Eq. 2 per head: ``errors``/``costs`` are ``[C, H]`` with row 0 the
+    baseline. Walking the candidates in order, the choice moves to any
+    candidate with a strictly lower error whose cost is not above the
+    baseline's (ties keep the earlier entry)."""
+    C, H = np.shape(errors)
     choice = []
     for h in range(H):
         best = 0
         for c in range(1, C):
-            if costs[c, h] <= costs[0, h] and errors[c, h] < errors[best, h]:
+            if costs[c][h] <= costs[0][h] and errors[c][h] < errors[best][h]:
                 best = c
         choice.append(best)
-    return {"configs": configs, "errors": errors, "costs": costs, "choice": choice,
-            "table": [configs[c] for c in choice]}
+    return choice
