@@ -118,9 +118,23 @@ def test_maximum_size_sampled(gpu_lib):
     the oracle."""
     import paper_2607_03612_amd as P
 
+    import torch
+
     w = Workload("max-8x131072", 8, 131072, "bf16", ("fixed", 0, 1, 1), heads=3)
     assert w.tokens == 1 << 20 and w.nb == 16384
     _sampled_check(P, w, 0, samples=6, seed=11)
+    # the single-launch selection (two score rows per workgroup at this size)
+    # gives the same lists as the workspace path checked above
+    q, k, _ = make_qkv(w)
+    table = make_table(w)
+    tq, tk = (PT.to_device(x, "bf16") for x in (q, k))
+    qp, kp = P.estimate_blocks(tq, tk, table, w.frames, w.tokens_per_frame)
+    got = []
+    for ws in (None, PT.select_workspace(P, table, w, heads=1)):
+        idx, cnt, _ = P.select_blocks(qp, kp, table, w.frames, w.tokens_per_frame, workspace=ws)
+        torch.cuda.synchronize()
+        got.append((idx[:2].cpu().numpy(), cnt.cpu().numpy()))  # the two Top-K heads
+    assert np.array_equal(got[0][1], got[1][1]) and np.array_equal(got[0][0], got[1][0])
 
 
 @pytest.mark.parametrize("name,layer", [("S4xT261-f32", 0), ("S8xT1374-bf16", 0),
