@@ -174,6 +174,175 @@ def measure_next_rows(P, torch, w, tq, tk, tv, out, table):
     return res
 
 
+def kept_flops_device(torch, idx, cnt, table, n, nb):
+    """kept_flops computed on the device (the index lists of the stack's
+    layers are hundreds of MB each); only per-head sums reach the host."""
+    last = n - (nb - 1) * 64
+    rows = torch.full((nb,), 64, dtype=torch.int64, device=cnt.device)
+    rows[-1] = last
+    slot = torch.arange(idx.shape[2], device=idx.device)
+    total = 0
+    for h, (pattern, _) in enumerate(table):
+        if pattern == 0:
+            total += 4 * n * n * 64
+            continue
+        c = cnt[h].to(torch.int64)
+        has_last = ((idx[h] == nb - 1) & (slot[None, :] < c[:, None])).any(dim=1).to(torch.int64)
+        keys = 64 * c - (64 - last) * has_last
+        total += int(4 * 64 * (rows * keys).sum().item())
+    return total
+
+
+def run_stack(args, P, torch, w):
+    """A stack of layers run end to end: every layer has fresh seeded Q/K/V
+    and its own seeded pattern table, all resident in HBM; a step is
+    estimation, selection and attention of every layer in order."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    from workloads import layer_tau, make_qkv, make_table
+
+    H, N, nb, S, T, L = w.heads, w.tokens, w.nb, w.frames, w.tokens_per_frame, w.layers
+    code = P.BF16 if w.dtype == "bf16" else P.F32
+
+    def up(x):
+        if w.dtype == "bf16":
+            return torch.from_numpy(x.view(np.int16)).cuda().view(torch.bfloat16)
+        return torch.from_numpy(x).cuda()
+
+    t0 = time.time()
+    layers, host0 = [], None
+    with ThreadPoolExecutor(2) as pool:
+        futs = [pool.submit(make_qkv, w, l, args.seed) for l in range(L)]
+        for l in range(L):
+            q, k, v = futs[l].result()
+            futs[l] = None
+            table = make_table(w, l, seed=args.seed)
+            layers.append({"q": up(q), "k": up(k), "v": up(v), "table": table,
+                           "cap": P.index_capacity(table, S, T, code),
+                           "tau": layer_tau(w, l, args.seed)})
+            if l == 0:
+                host0 = (q, k, v)
+            del q, k, v
+            log(f"[stack] layer {l}: tau {layers[-1]['tau']}% cap {layers[-1]['cap']} "
+                f"({time.time() - t0:.1f}s)")
+    dev = layers[0]["q"].device
+    qp = torch.zeros((H, nb, 64), dtype=torch.float64, device=dev)
+    kp = torch.zeros((H, 64, nb), dtype=torch.float64, device=dev)
+    idx_buf = torch.empty(H * nb * max(x["cap"] for x in layers), dtype=torch.int32, device=dev)
+    cnt = torch.empty((H, nb), dtype=torch.int32, device=dev)
+    ws_bytes = max(P.select_workspace_bytes(x["table"], S, T, code) for x in layers)
+    sel_ws = torch.empty(max(ws_bytes, 16) // 4, dtype=torch.int32, device=dev)
+    out = torch.empty_like(layers[0]["q"])
+
+    def run_layer(x, ev=None):
+        idx = idx_buf[: H * nb * x["cap"]].view(H, nb, x["cap"])
+        if ev:
+            ev[0].record()
+        P.estimate_blocks(x["q"], x["k"], x["table"], S, T, qp, kp)
+        if ev:
+            ev[1].record()
+        P.select_blocks(qp, kp, x["table"], S, T, x["cap"], idx, cnt, dtype=code, workspace=sel_ws)
+        if ev:
+            ev[2].record()
+        P.sparse_attention(x["q"], x["k"], x["v"], x["table"], S, T, idx, cnt, out)
+        if ev:
+            ev[3].record()
+        return idx
+
+    # algorithmic FLOP and achieved sparsity of every layer, outside the timing
+    for x in layers:
+        idx = run_layer(x)
+        x["flop"] = kept_flops_device(torch, idx, cnt, x["table"], N, nb)
+        c = cnt.to(torch.int64)
+        x["pairs"] = sum(nb * nb if p == 0 else int(c[h].sum().item())
+                         for h, (p, _) in enumerate(x["table"]))
+    torch.cuda.synchronize()
+
+    def step(evs=None):
+        for l, x in enumerate(layers):
+            run_layer(x, evs[l] if evs else None)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [[[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(L)]
+           for _ in range(args.steps)]
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for s in range(args.steps):
+        step(evs[s])
+    end.record()
+    torch.cuda.synchronize()
+    ms_step = start.elapsed_time(end) / args.steps
+
+    per_layer, att_total, flop_total, ph = [], 0.0, 0, np.zeros(3)
+    for l, x in enumerate(layers):
+        t = np.array([[e[l][i].elapsed_time(e[l][i + 1]) for i in range(3)] for e in evs]).mean(axis=0)
+        ph += t
+        att_total += t[2]
+        flop_total += x["flop"]
+        tab = x["table"]
+        per_layer.append({"layer": l, "tau_percent": x["tau"],
+                          "table": {"dense": sum(p == 0 for p, _ in tab),
+                                    "frame_local": sum(p == 1 for p, _ in tab),
+                                    "topk_blocks": sorted({k for p, k in tab if p == 2})},
+                          "sparsity": round(1.0 - x["pairs"] / (H * nb * nb), 4),
+                          "ms": [round(float(v), 4) for v in t],
+                          "attention_tflops": round(x["flop"] / (t[2] * 1e-3) / 1e12, 1)})
+    flops_dense = 4 * N * N * 64 * H
+    peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
+    att_tflops = flop_total / (att_total * 1e-3) / 1e12
+    log(f"[stack] {L} layers: {ms_step:.2f} ms per step ({ms_step / L:.3f} ms per layer); "
+        f"estimate {ph[0]:.2f}, select {ph[1]:.2f}, attention {ph[2]:.2f} ms; "
+        f"attention {att_tflops:.1f} TFLOP/s")
+
+    cpu = None
+    if args.cpu_rows > 0:
+        rows = min(args.cpu_rows, 16)
+        t0 = time.perf_counter()
+        sec, rows = oracle_sample(w, *host0, layers[0]["table"], rows, seed=args.seed)
+        wall = time.perf_counter() - t0
+        cpu = {"value": round(flops_dense / sec / 1e12, 6), "unit": "dense-equiv TFLOP/s",
+               "cores": blas_threads(), "kind": "oracle",
+               "ms_per_layer": round(sec * 1e3, 1),
+               "sample": f"layer 0 only: {rows} of {nb} query blocks per head (seeded), all "
+                         f"{H} heads; per-head work timed in full, per-block work scaled by "
+                         f"{nb}/{rows}; {wall:.1f} s of CPU work"}
+        log(f"[stack] cpu oracle {cpu}")
+
+    result = {
+        "metric": METRIC,
+        "value": round(L * flops_dense / (ms_step * 1e-3) / 1e12, 2),
+        "unit": "dense-equiv TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "ms_per_layer": round(ms_step / L, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {"workload": w.name, "layers": L, "frames": S, "tokens_per_frame": T,
+                   "tokens": N, "heads": H, "head_dim": 64, "block": 64, "key_blocks": nb,
+                   "achieved_block_sparsity": round(
+                       1.0 - sum(x["pairs"] for x in layers) / (L * H * nb * nb), 4)},
+        "roofline": {
+            "kernel": "attn_bf16_kernel" if w.dtype == "bf16" else "attn_f32_kernel",
+            "bound": "mfma", "achieved": round(att_tflops, 2), "peak": peak, "unit": "TFLOP/s",
+            "frac": round(att_tflops / peak, 4), "traffic": None,
+            "flop_per_step": flop_total, "attention_ms_per_step": round(att_total, 4),
+        },
+        "kernels_ms_per_step": {"estimate": round(float(ph[0]), 4), "select": round(float(ph[1]), 4),
+                                "attention": round(float(ph[2]), 4)},
+        "per_layer": per_layer,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(result), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -221,6 +390,9 @@ def main():
         raise SystemExit("no GPU visible: the HIP path needs an MI355X")
 
     w = WORKLOADS[args.workload]
+    if w.layers > 1:
+        run_stack(args, P, torch, w)
+        return
     t0 = time.time()
     q, k, v = make_qkv(w, seed=args.seed)
     table = make_table(w, seed=args.seed)
