@@ -232,6 +232,8 @@ def run_stack(args, P, torch, w):
     cnt = torch.empty((H, nb), dtype=torch.int32, device=dev)
     ws_bytes = max(P.select_workspace_bytes(x["table"], S, T, code) for x in layers)
     sel_ws = torch.empty(max(ws_bytes, 16) // 4, dtype=torch.int32, device=dev)
+    att_bytes = max(P.attention_workspace_bytes(x["table"], S, T, code) for x in layers)
+    att_ws = torch.empty(max(att_bytes, 16) // 4, dtype=torch.int32, device=dev) if args.split else None
     out = torch.empty_like(layers[0]["q"])
 
     def run_layer(x, ev=None):
@@ -244,7 +246,8 @@ def run_stack(args, P, torch, w):
         P.select_blocks(qp, kp, x["table"], S, T, x["cap"], idx, cnt, dtype=code, workspace=sel_ws)
         if ev:
             ev[2].record()
-        P.sparse_attention(x["q"], x["k"], x["v"], x["table"], S, T, idx, cnt, out)
+        P.sparse_attention(x["q"], x["k"], x["v"], x["table"], S, T, idx, cnt, out,
+                           workspace=att_ws)
         if ev:
             ev[3].record()
         return idx
@@ -288,6 +291,7 @@ def run_stack(args, P, torch, w):
                                     "frame_local": sum(p == 1 for p, _ in tab),
                                     "topk_blocks": sorted({k for p, k in tab if p == 2})},
                           "sparsity": round(1.0 - x["pairs"] / (H * nb * nb), 4),
+                          "attention_workspace_bytes": P.attention_workspace_bytes(tab, S, T, code),
                           "ms": [round(float(v), 4) for v in t],
                           "attention_tflops": round(x["flop"] / (t[2] * 1e-3) / 1e12, 1)})
     flops_dense = 4 * N * N * 64 * H
@@ -325,7 +329,8 @@ def run_stack(args, P, torch, w):
         "vs_baseline": None,
         "dtype": w.dtype,
         "data": "synthetic",
-        "config": {"workload": w.name, "layers": L, "frames": S, "tokens_per_frame": T,
+        "config": {"workload": w.name, "layers": L, "split_long_lists": bool(args.split),
+                   "frames": S, "tokens_per_frame": T,
                    "tokens": N, "heads": H, "head_dim": 64, "block": 64, "key_blocks": nb,
                    "achieved_block_sparsity": round(
                        1.0 - sum(x["pairs"] for x in layers) / (L * H * nb * nb), 4)},
@@ -355,6 +360,9 @@ def main():
                     help="query blocks per head in the oracle CPU sample (0 = skip)")
     ap.add_argument("--next-rows", type=int, default=1,
                     help="also time the stride, global-probe, cosine and NMSE kernels (0 = skip)")
+    ap.add_argument("--split", type=int, default=1, choices=(0, 1),
+                    help="1: pass the attention workspace, so lists of 384+ key blocks run split "
+                         "into key ranges; 0: the unsplit launch (same work and results)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run three device-to-device copies of MIB MiB (a plain copy "
                          "kernel of known size, to scale rocprofv3 FETCH_SIZE / WRITE_SIZE) and exit")
@@ -417,6 +425,10 @@ def main():
     # single launch that keeps score rows in LDS; the same lists)
     sel_ws_bytes = P.select_workspace_bytes(table, S, T, code)
     sel_ws = torch.empty(max(sel_ws_bytes, 16) // 4, dtype=torch.int32, device=dev)
+    # long lists (384+ key blocks) run split into key ranges through a
+    # workspace; none at this layer's budget, the call takes it all the same
+    att_ws_bytes = P.attention_workspace_bytes(table, S, T, code)
+    att_ws = torch.empty(max(att_ws_bytes, 16) // 4, dtype=torch.int32, device=dev) if args.split else None
 
     def step(ev=None):
         if ev:
@@ -427,7 +439,7 @@ def main():
         P.select_blocks(qp, kp, table, S, T, cap, idx, cnt, dtype=code, workspace=sel_ws)
         if ev:
             ev[2].record()
-        P.sparse_attention(tq, tk, tv, table, S, T, idx, cnt, out)
+        P.sparse_attention(tq, tk, tv, table, S, T, idx, cnt, out, workspace=att_ws)
         if ev:
             ev[3].record()
 

@@ -201,11 +201,32 @@ int64_t saf3r_select_workspace_bytes(const saf3r_problem* problem, const saf3r_h
  *                gives unspecified output values but no out-of-bounds access.
  *   out          device [heads, N, 64] of problem->dtype
  *   lse_or_null  NULL, or device float32 [heads, N]
+ *   workspace_or_null, workspace_bytes
+ *                NULL: every query block of a head is one work item. A
+ *                device buffer (16-byte aligned) of at least
+ *                saf3r_attention_workspace_bytes(problem, table) bytes
+ *                (else SAF3R_ERR_CAPACITY): bf16 list heads whose list can
+ *                hold 384 or more key blocks run as 4 items per query block,
+ *                one per quarter of the key range, and a second launch merges
+ *                the 4 partial softmax results per query in a fixed order
+ *                (results differ from the unsplit launch only by fp32
+ *                rounding and the bf16 rounding of P against each range's
+ *                running max). Lists that are not ascending are still read
+ *                within their row. The buffer is overwritten; launches that
+ *                share one must be ordered on the GPU.
  * Returns SAF3R_OK, or an error with nothing enqueued. */
 saf3r_status saf3r_sparse_attention(const saf3r_problem* problem, const saf3r_head_cfg* table,
                                     const void* q, const void* k, const void* v,
                                     const int32_t* block_idx, const int32_t* block_cnt, int32_t cap,
-                                    void* out, float* lse_or_null, void* stream);
+                                    void* out, float* lse_or_null, void* workspace_or_null,
+                                    int64_t workspace_bytes, void* stream);
+
+/* Workspace of saf3r_sparse_attention that splits its long lists:
+ * (split heads) x 4 x nb x 16896 bytes, where the split heads are the bf16
+ * FRAME_LOCAL / TOPK / ANCHOR / GLOBAL_PROBE / COSINE_TOPK heads whose list
+ * can hold 384 or more key blocks (2.9 GB for 10 such heads at nb = 4294);
+ * 0 if there are none; or a negative saf3r_status. */
+int64_t saf3r_attention_workspace_bytes(const saf3r_problem* problem, const saf3r_head_cfg* table);
 
 /* Workspace bytes saf3r_cosine_select needs for features of width
  * feat_dim: (feat_dim * nb + nb * nb) * 8, or a negative saf3r_status. */

@@ -14,6 +14,7 @@ from .binding import (  # noqa: F401
     GLOBAL_PROBE,
     TOPK,
     Saf3rError,
+    attention_workspace_bytes,
     cosine_select,
     cosine_workspace_bytes,
     estimate_blocks,

@@ -24,6 +24,7 @@ EXPORTS = (
     "saf3r_select_blocks",
     "saf3r_select_workspace_bytes",
     "saf3r_sparse_attention",
+    "saf3r_attention_workspace_bytes",
     "saf3r_cosine_workspace_bytes",
     "saf3r_cosine_select",
     "saf3r_nmse_workspace_bytes",
@@ -63,8 +64,10 @@ def _declare(lib):
     lib.saf3r_select_blocks.restype = I32
     lib.saf3r_select_workspace_bytes.argtypes = [P, C]
     lib.saf3r_select_workspace_bytes.restype = ctypes.c_int64
-    lib.saf3r_sparse_attention.argtypes = [P, C, V, V, V, V, V, I32, V, V, V]
+    lib.saf3r_sparse_attention.argtypes = [P, C, V, V, V, V, V, I32, V, V, V, ctypes.c_int64, V]
     lib.saf3r_sparse_attention.restype = I32
+    lib.saf3r_attention_workspace_bytes.argtypes = [P, C]
+    lib.saf3r_attention_workspace_bytes.restype = ctypes.c_int64
     lib.saf3r_cosine_workspace_bytes.argtypes = [P, I32]
     lib.saf3r_cosine_workspace_bytes.restype = ctypes.c_int64
     lib.saf3r_cosine_select.argtypes = [P, C, V, I32, V, ctypes.c_int64, V, V, I32, V]
@@ -222,9 +225,22 @@ def select_blocks(q_pooled, k_pooled, table, frames, tokens_per_frame, cap=None,
     return block_idx, block_cnt, scores
 
 
+def attention_workspace_bytes(table, frames, tokens_per_frame, dtype=BF16) -> int:
+    """Bytes of the workspace that lets saf3r_sparse_attention split its long
+    lists into key ranges (0 if no head qualifies)."""
+    p = problem(len(table), frames, tokens_per_frame, dtype)
+    r = _lib().saf3r_attention_workspace_bytes(ctypes.byref(p), head_table(table))
+    _check(min(r, 0), "saf3r_attention_workspace_bytes")
+    return int(r)
+
+
 def sparse_attention(q, k, v, table, frames, tokens_per_frame, block_idx=None, block_cnt=None,
-                     out=None, want_lse=False, stream=None):
-    """Attention over the kept keys: ``(out [H, N, 64], lse [H, N] float32 or None)``."""
+                     out=None, want_lse=False, workspace=None, stream=None):
+    """Attention over the kept keys: ``(out [H, N, 64], lse [H, N] float32 or None)``.
+
+    ``workspace``: None, or a contiguous device tensor (any dtype, 16-byte
+    aligned) of at least ``attention_workspace_bytes`` bytes, with which long
+    lists run split into key ranges."""
     import torch
 
     _check_qkv(q, k, v)
@@ -236,9 +252,11 @@ def sparse_attention(q, k, v, table, frames, tokens_per_frame, block_idx=None, b
         out = torch.empty_like(q)
     lse = torch.empty((H, N), dtype=torch.float32, device=q.device) if want_lse else None
     p = problem(H, frames, tokens_per_frame, _torch_dtype_code(q))
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _check(_lib().saf3r_sparse_attention(ctypes.byref(p), head_table(table), _ptr(q), _ptr(k),
                                          _ptr(v), _ptr(block_idx), _ptr(block_cnt), cap, _ptr(out),
-                                         _ptr(lse), _stream(stream)),
+                                         _ptr(lse), _ptr(workspace), ctypes.c_int64(ws_bytes),
+                                         _stream(stream)),
            "saf3r_sparse_attention")
     return out, lse
 

@@ -259,10 +259,49 @@ saf3r_status saf3r_select_blocks(const saf3r_problem* problem, const saf3r_head_
   return SAF3R_OK;
 }
 
+// Key blocks one query block of head h walks (its work if not split).
+static int attention_cost(const Shape& s, const saf3r_head_cfg* table, int h, int fl_len) {
+  const int p = table[h].pattern;
+  switch (p) {
+    case SAF3R_DENSE: return s.nb;
+    case SAF3R_FRAME_LOCAL: return fl_len;
+    case SAF3R_ANCHOR: return anchor_len(s, table[h].param);
+    case SAF3R_COSINE_TOPK: return cosine_len(s, table[h].param);
+    case SAF3R_STRIDE:
+      return (int)((((s.n + table[h].param - 1) / table[h].param) + saf3r::kBlock - 1) /
+                   saf3r::kBlock);
+    default: return table[h].param;  // TOPK, GLOBAL_PROBE
+  }
+}
+
+// A list head whose list can reach kSplitMinBlocks key blocks runs split
+// into key ranges (bf16 only).
+static bool attention_split(const Shape& s, const saf3r_head_cfg* table, int h, int cost) {
+  const int p = table[h].pattern;
+  const bool listed = p == SAF3R_FRAME_LOCAL || p == SAF3R_TOPK || p == SAF3R_ANCHOR ||
+                      p == SAF3R_GLOBAL_PROBE || p == SAF3R_COSINE_TOPK;
+  return listed && s.dtype == SAF3R_BF16 && cost >= saf3r::kSplitMinBlocks;
+}
+
+int64_t saf3r_attention_workspace_bytes(const saf3r_problem* problem, const saf3r_head_cfg* table) {
+  Shape s;
+  saf3r_status st = check_problem(problem, &s);
+  if (st != SAF3R_OK) return st;
+  st = check_table(s, table);
+  if (st != SAF3R_OK) return st;
+  const int fl_len = max_frame_local_len(s);
+  int64_t n_split = 0;
+  for (int h = 0; h < s.heads; ++h)
+    n_split += attention_split(s, table, h, attention_cost(s, table, h, fl_len)) ? 1 : 0;
+  return n_split * saf3r::kSplitChunks * s.nb * saf3r::kSplitItemBytes;
+}
+
 saf3r_status saf3r_sparse_attention(const saf3r_problem* problem, const saf3r_head_cfg* table,
                                     const void* q, const void* k, const void* v,
                                     const int32_t* block_idx, const int32_t* block_cnt,
-                                    int32_t cap, void* out, float* lse_or_null, void* stream) {
+                                    int32_t cap, void* out, float* lse_or_null,
+                                    void* workspace_or_null, int64_t workspace_bytes,
+                                    void* stream) {
   Shape s;
   saf3r_status st = check_problem(problem, &s);
   if (st != SAF3R_OK) return st;
@@ -278,18 +317,28 @@ saf3r_status saf3r_sparse_attention(const saf3r_problem* problem, const saf3r_he
     if (!block_idx || !block_cnt) return SAF3R_ERR_INVALID_ARGUMENT;
     if (cap < capacity(s, table)) return SAF3R_ERR_CAPACITY;
   }
+  const int64_t split_bytes = saf3r_attention_workspace_bytes(problem, table);
+  if (split_bytes < 0) return (saf3r_status)split_bytes;
+  const bool split = workspace_or_null != nullptr && split_bytes > 0;
+  if (workspace_or_null) {
+    if (workspace_bytes < split_bytes) return SAF3R_ERR_CAPACITY;
+    if (reinterpret_cast<uintptr_t>(workspace_or_null) % 16 != 0) return SAF3R_ERR_INVALID_ARGUMENT;
+  }
 
-  // Two launches: heads with block lists or dense (one kernel, heads in
-  // decreasing per-row cost so the longest rows start first), then STRIDE
-  // heads (token-sampled keys).
+  // Up to three launches: heads with block lists or dense (one kernel, work
+  // items in decreasing length so the longest start first; split heads as
+  // kSplitChunks items per query block), the merge of split heads, then
+  // STRIDE heads (token-sampled keys).
   saf3r::AttnArgs a{};
   a.n = s.n;
   a.nb = s.nb;
   a.cap = cap;
   a.slab = (s.nb + 7) / 8;
+  a.splits = saf3r::kSplitChunks;
   a.scale_log2 = (float)(1.4426950408889634 / sqrt((double)saf3r::kHeadDim));
   saf3r::AttnArgs sa = a;
-  std::vector<int> cost(s.heads, 0);
+  std::vector<int> item_cost(s.heads, 0);
+  std::vector<char> is_split(s.heads, 0);
   const int fl_len = max_frame_local_len(s);
   std::vector<int> listed, strided;
   bool all_dense = true;
@@ -298,16 +347,9 @@ saf3r_status saf3r_sparse_attention(const saf3r_problem* problem, const saf3r_he
     if (p == SAF3R_SKIP) continue;
     a.dense[h] = p == SAF3R_DENSE ? 1 : 0;
     sa.stride[h] = p == SAF3R_STRIDE ? table[h].param : 1;
-    switch (p) {
-      case SAF3R_DENSE: cost[h] = s.nb; break;
-      case SAF3R_FRAME_LOCAL: cost[h] = fl_len; break;
-      case SAF3R_ANCHOR: cost[h] = anchor_len(s, table[h].param); break;
-      case SAF3R_COSINE_TOPK: cost[h] = cosine_len(s, table[h].param); break;
-      case SAF3R_STRIDE:
-        cost[h] = (int)((((s.n + table[h].param - 1) / table[h].param) + saf3r::kBlock - 1) / saf3r::kBlock);
-        break;
-      default: cost[h] = table[h].param; break;  // TOPK, GLOBAL_PROBE
-    }
+    const int cost = attention_cost(s, table, h, fl_len);
+    is_split[h] = split && attention_split(s, table, h, cost) ? 1 : 0;
+    item_cost[h] = is_split[h] ? (cost + saf3r::kSplitChunks - 1) / saf3r::kSplitChunks : cost;
     if (p == SAF3R_STRIDE) {
       strided.push_back(h);
     } else {
@@ -315,20 +357,45 @@ saf3r_status saf3r_sparse_attention(const saf3r_problem* problem, const saf3r_he
       all_dense = all_dense && p == SAF3R_DENSE;
     }
   }
-  auto by_cost = [&](int x, int y) { return cost[x] > cost[y]; };
+  auto by_cost = [&](int x, int y) { return item_cost[x] > item_cost[y]; };
   std::stable_sort(listed.begin(), listed.end(), by_cost);
   std::stable_sort(strided.begin(), strided.end(), by_cost);
+  saf3r::MergeArgs ma{};
+  ma.n = s.n;
+  ma.nb = s.nb;
+  ma.splits = saf3r::kSplitChunks;
   a.heads = (int)listed.size();
   a.mode = all_dense ? 1 : 0;
-  for (size_t i = 0; i < listed.size(); ++i) a.order[i] = (int16_t)listed[i];
+  a.unit_start[0] = 0;
+  for (size_t i = 0; i < listed.size(); ++i) {
+    const int h = listed[i];
+    a.order[i] = (int16_t)h;
+    a.split_pos[i] = is_split[h] ? (int16_t)ma.n_split : (int16_t)-1;
+    if (is_split[h]) ma.head[ma.n_split++] = (int16_t)h;
+    a.unit_start[i + 1] = a.unit_start[i] + a.slab * (is_split[h] ? saf3r::kSplitChunks : 1);
+  }
+  const int64_t part_o_bytes =
+      (int64_t)ma.n_split * saf3r::kSplitChunks * s.nb * saf3r::kBlock * saf3r::kHeadDim * 4;
+  a.part_o = split ? static_cast<float*>(workspace_or_null) : nullptr;
+  a.part_ml = split ? reinterpret_cast<float*>(static_cast<char*>(workspace_or_null) + part_o_bytes)
+                    : nullptr;
   sa.heads = (int)strided.size();
   sa.mode = 2;
-  for (size_t i = 0; i < strided.size(); ++i) sa.order[i] = (int16_t)strided[i];
+  sa.unit_start[0] = 0;
+  for (size_t i = 0; i < strided.size(); ++i) {
+    sa.order[i] = (int16_t)strided[i];
+    sa.split_pos[i] = -1;
+    sa.unit_start[i + 1] = sa.unit_start[i] + sa.slab;
+  }
 
   hipStream_t hs = static_cast<hipStream_t>(stream);
   hipError_t e = saf3r::launch_attention(s.dtype, q, k, v, block_idx, block_cnt, out, lse_or_null,
                                          a, hs);
   if (e != hipSuccess) return SAF3R_ERR_HIP;
+  if (ma.n_split > 0) {
+    e = saf3r::launch_attention_merge(a.part_o, a.part_ml, out, lse_or_null, ma, hs);
+    if (e != hipSuccess) return SAF3R_ERR_HIP;
+  }
   return hip_status(saf3r::launch_attention(s.dtype, q, k, v, block_idx, block_cnt, out,
                                             lse_or_null, sa, hs));
 }

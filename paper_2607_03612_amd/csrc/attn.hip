@@ -58,18 +58,35 @@ __device__ inline float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 struct Work {
   int h, i;
+  int chunk;  // key range of a split head's item, or -1
+  int item;   // split item index (partials), or -1
   bool valid;
 };
 
+// Work unit u = b / 8 of order position hh covers unit_start[hh] <= u <
+// unit_start[hh + 1]: slab units per key range, key ranges in order, so the
+// items that run together on an XCD share one key range of one head.
 __device__ inline Work work_item(const AttnArgs& a) {
   const int xcd = blockIdx.x & 7;
   const int u = blockIdx.x >> 3;
-  const int hh = u / a.slab;
-  const int i = xcd * a.slab + (u - hh * a.slab);
   Work w;
-  w.valid = hh < a.heads && i < a.nb;
-  w.h = w.valid ? a.order[hh] : 0;
+  w.valid = u < a.unit_start[a.heads];
+  if (!w.valid) return w;
+  int lo = 0, hi = a.heads;  // the last order position with unit_start <= u
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (a.unit_start[mid] <= u) lo = mid;
+    else hi = mid;
+  }
+  const int r = u - a.unit_start[lo];
+  const int chunk = r / a.slab;
+  const int i = xcd * a.slab + (r - chunk * a.slab);
+  w.valid = i < a.nb;
+  w.h = a.order[lo];
   w.i = i;
+  const int sp = a.split_pos[lo];
+  w.chunk = sp >= 0 ? chunk : -1;
+  w.item = sp >= 0 ? (sp * a.splits + chunk) * a.nb + i : -1;
   return w;
 }
 
@@ -155,6 +172,44 @@ __device__ inline void dma_half_strided(__amdgpu_buffer_rsrc_t r, int j, int h, 
   }
 }
 
+// Output of one query block from the O^T accumulators (register e of tile
+// [c][tq] of lane (l32, hf) holds head dim 32c + 8(e/4) + 4hf + e%4 of query
+// 32tq + l32): scaled by inv, rounded to bf16 into two idle LDS half buffers
+// (query rows 0..31 in b0, 32..63 in b1, same swizzle as the K tiles), then
+// stored as full 128-byte rows, eight 1 KB stores. lse_row, if not null, is
+// the head's LSE row; lse_val is in natural log.
+__device__ inline void write_out_tile(const f32x16 (&o)[2][2], const float (&inv)[2],
+                                      const float (&lse_val)[2], lds_char* b0, lds_char* b1,
+                                      __amdgpu_buffer_rsrc_t ro, float* lse_row, int i, int64_t n,
+                                      int lane) {
+  const int l32 = lane & 31;
+  const int hf = lane >> 5;
+#pragma unroll
+  for (int tq = 0; tq < 2; ++tq) {
+    const int query = i * kBlock + 32 * tq + l32;
+    lds_char* const ob = tq ? b1 : b0;
+#pragma unroll
+    for (int c = 0; c < 2; ++c)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        bf16x4 ov;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) ov[r] = (__bf16)(o[c][tq][4 * g + r] * inv[tq]);
+        *(lds_bf16x4*)(ob + swz(l32, 4 * c + g) + 8 * hf) = ov;
+      }
+    if (lse_row && hf == 0 && query < n) lse_row[query] = lse_val[tq];
+  }
+#pragma unroll
+  for (int nn = 0; nn < 8; ++nn) {
+    const int row = 8 * nn + (lane >> 3);
+    const int chunk = lane & 7;
+    lds_char* const ob = row >= 32 ? b1 : b0;
+    const bf16x8 val = *(lds_bf16x8*)(ob + swz(row & 31, chunk));
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(i32x4, val), ro,
+                                           (int)(((i * kBlock + row) * kHeadDim + 8 * chunk) * 2), 0, 0);
+  }
+}
+
 template <int kMode>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_bf16_kernel(const uint16_t* __restrict__ q,
                                                       const uint16_t* __restrict__ k,
@@ -188,6 +243,24 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
   const int64_t nkeys = kMode == kStrided ? (a.n + stride - 1) / stride : a.n;
   int count = kMode == kStrided ? (int)((nkeys + kBlock - 1) / kBlock) : nb;
   if (!dense) count = min(max(cnt[(int64_t)w.h * nb + w.i], 0), a.cap);
+  if constexpr (kMode == kLists) {
+    if (w.chunk >= 0 && !dense) {
+      // this item's key range [jlo, jhi): in an ascending list, the entries
+      // after those below jlo and before the first at or above jhi (any other
+      // list still yields a sub-range of the row)
+      const int jlo = (int)(((int64_t)w.chunk * nb) / a.splits);
+      const int jhi = (int)(((int64_t)(w.chunk + 1) * nb) / a.splits);
+      int below_lo = 0, below_hi = 0;
+      for (int base = 0; base < count; base += 64) {
+        const int p = base + lane;
+        const int j = p < count ? list[p] : 0x7fffffff;
+        below_lo += __popcll(__ballot(j < jlo));
+        below_hi += __popcll(__ballot(j < jhi));
+      }
+      list += below_lo;
+      count = max(below_hi - below_lo, 0);
+    }
+  }
 
   const int64_t head_off = (int64_t)w.h * a.n * kHeadDim;
   const uint32_t head_bytes = (uint32_t)(a.n * kHeadDim * 2);
@@ -230,6 +303,16 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
   float l[2] = {0.f, 0.f};          // this lane's share of the running row sum
 
   if (count <= 0) {  // an empty list: no keys, zero output, LSE -inf
+    if constexpr (kMode == kLists) {
+      if (w.chunk >= 0) {  // an empty key range: statistics only, the merge skips it
+        if (hf == 0) {
+#pragma unroll
+          for (int tq = 0; tq < 2; ++tq)
+            *(f32x2*)(a.part_ml + ((int64_t)w.item * kBlock + 32 * tq + l32) * 2) = f32x2{kNegInf, 0.f};
+        }
+        return;
+      }
+    }
 #pragma unroll
     for (int tq = 0; tq < 2; ++tq) {
       const int query = w.i * kBlock + 32 * tq + l32;
@@ -475,36 +558,99 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
     mfma_pv(vA, p_new);
   }
 
-  // epilogue: normalise and round to bf16 into the (now idle) K half buffers
-  // (query rows 0..31 in one, 32..63 in the other, same swizzle), then store
-  // full 128-byte rows: eight 1 KB stores; log-sum-exp in natural log
+  float lt[2];
+#pragma unroll
+  for (int tq = 0; tq < 2; ++tq) lt[tq] = pair_sum(l[tq]);
+  if constexpr (kMode == kLists) {
+    if (w.chunk >= 0) {
+      // a split item: O^T accumulators as they stand (register-major, 1 KB
+      // per store instruction) and (running max, row sum) per query
+      float* const po = a.part_o + (int64_t)w.item * (kBlock * kHeadDim);
+#pragma unroll
+      for (int c = 0; c < 2; ++c)
+#pragma unroll
+        for (int tq = 0; tq < 2; ++tq)
+#pragma unroll
+          for (int g = 0; g < 4; ++g)
+            *(f32x4*)(po + (((c * 2 + tq) * 4 + g) * 64 + lane) * 4) =
+                f32x4{o[c][tq][4 * g], o[c][tq][4 * g + 1], o[c][tq][4 * g + 2], o[c][tq][4 * g + 3]};
+      if (hf == 0) {
+#pragma unroll
+        for (int tq = 0; tq < 2; ++tq)
+          *(f32x2*)(a.part_ml + ((int64_t)w.item * kBlock + 32 * tq + l32) * 2) = f32x2{m[tq], lt[tq]};
+      }
+      return;
+    }
+  }
+  const float inv[2] = {1.0f / lt[0], 1.0f / lt[1]};
+  const float lse_val[2] = {(m[0] + __log2f(lt[0])) * kLn2, (m[1] + __log2f(lt[1])) * kLn2};
+  write_out_tile(o, inv, lse_val, kbuf0, kbuf1, ro, lse ? lse + (int64_t)w.h * a.n : nullptr, w.i,
+                 a.n, lane);
+}
+
+// Combines the key ranges of split heads: per query, M = max of the ranges'
+// running maxima, weights 2^(m_c - M), O = sum_c w_c O_c / sum_c w_c l_c, in
+// range order. One wave per (split head, query block).
+__global__ __launch_bounds__(64) void attn_merge_kernel(const float* __restrict__ part_o,
+                                                       const float* __restrict__ part_ml,
+                                                       uint16_t* __restrict__ out,
+                                                       float* __restrict__ lse, MergeArgs a) {
+  __shared__ __attribute__((aligned(1024))) char b0[32 * 128];
+  __shared__ __attribute__((aligned(1024))) char b1[32 * 128];
+  const int sp = blockIdx.x / a.nb;
+  const int i = blockIdx.x - sp * a.nb;
+  if (sp >= a.n_split) return;
+  const int h = a.head[sp];
+  const int lane = threadIdx.x;
+  const int l32 = lane & 31;
+  auto ml_at = [&](int c, int tq) -> f32x2 {
+    const int64_t item = (int64_t)(sp * a.splits + c) * a.nb + i;
+    return *(const f32x2*)(part_ml + (item * kBlock + 32 * tq + l32) * 2);
+  };
+  float mx[2] = {kNegInf, kNegInf};
+  for (int c = 0; c < a.splits; ++c)
+#pragma unroll
+    for (int tq = 0; tq < 2; ++tq) mx[tq] = fmaxf(mx[tq], ml_at(c, tq)[0]);
+  float lt[2] = {0.f, 0.f};
+  f32x16 o[2][2];
+#pragma unroll
+  for (int c = 0; c < 2; ++c)
+#pragma unroll
+    for (int tq = 0; tq < 2; ++tq)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) o[c][tq][e] = 0.f;
+  for (int c = 0; c < a.splits; ++c) {
+    float wgt[2];
+#pragma unroll
+    for (int tq = 0; tq < 2; ++tq) {
+      const f32x2 ml = ml_at(c, tq);
+      wgt[tq] = ml[0] == kNegInf ? 0.f : fast_exp2(ml[0] - mx[tq]);
+      lt[tq] = fmaf(wgt[tq], ml[1], lt[tq]);
+    }
+    // an empty range (every query's max is -inf) wrote no accumulators
+    if (!__ballot(wgt[0] != 0.f || wgt[1] != 0.f)) continue;
+    const float* const po = part_o + ((int64_t)(sp * a.splits + c) * a.nb + i) * (kBlock * kHeadDim);
+#pragma unroll
+    for (int c2 = 0; c2 < 2; ++c2)
+#pragma unroll
+      for (int tq = 0; tq < 2; ++tq)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const f32x4 val = *(const f32x4*)(po + (((c2 * 2 + tq) * 4 + g) * 64 + lane) * 4);
+#pragma unroll
+          for (int r = 0; r < 4; ++r) o[c2][tq][4 * g + r] = fmaf(wgt[tq], val[r], o[c2][tq][4 * g + r]);
+        }
+  }
+  float inv[2], lse_val[2];
 #pragma unroll
   for (int tq = 0; tq < 2; ++tq) {
-    const float lt = pair_sum(l[tq]);
-    const float inv = 1.0f / lt;
-    const int query = w.i * kBlock + 32 * tq + l32;
-    lds_char* const ob = tq ? kbuf1 : kbuf0;
-#pragma unroll
-    for (int c = 0; c < 2; ++c)
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        bf16x4 ov;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) ov[r] = (__bf16)(o[c][tq][4 * g + r] * inv);
-        *(lds_bf16x4*)(ob + swz(l32, 4 * c + g) + 8 * hf) = ov;
-      }
-    if (lse && hf == 0 && query < a.n)
-      lse[(int64_t)w.h * a.n + query] = (m[tq] + __log2f(lt)) * kLn2;
+    inv[tq] = lt[tq] > 0.f ? 1.0f / lt[tq] : 0.f;
+    lse_val[tq] = lt[tq] > 0.f ? (mx[tq] + __log2f(lt[tq])) * kLn2 : kNegInf;
   }
-#pragma unroll
-  for (int n = 0; n < 8; ++n) {
-    const int row = 8 * n + (lane >> 3);
-    const int chunk = lane & 7;
-    lds_char* const ob = row >= 32 ? kbuf1 : kbuf0;
-    const bf16x8 val = *(lds_bf16x8*)(ob + swz(row & 31, chunk));
-    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(i32x4, val), ro,
-                                           (int)(((w.i * kBlock + row) * kHeadDim + 8 * chunk) * 2), 0, 0);
-  }
+  const int64_t head_off = (int64_t)h * a.n * kHeadDim;
+  const __amdgpu_buffer_rsrc_t ro = make_rsrc(out + head_off, (uint32_t)(a.n * kHeadDim * 2));
+  write_out_tile(o, inv, lse_val, (lds_char*)b0, (lds_char*)b1, ro,
+                 lse ? lse + (int64_t)h * a.n : nullptr, i, a.n, lane);
 }
 
 // ------------------------------------------------------------------ fp32
@@ -687,7 +833,7 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(const float* __restrict__ 
 hipError_t launch_attention(int dtype, const void* q, const void* k, const void* v,
                             const int32_t* idx, const int32_t* cnt, void* out, float* lse,
                             const AttnArgs& a, hipStream_t s) {
-  const int64_t groups = 8LL * a.heads * a.slab;
+  const int64_t groups = 8LL * a.unit_start[a.heads];
   if (groups == 0) return hipSuccess;
   const dim3 grid((unsigned)groups);
   if (dtype == 1) {
@@ -702,6 +848,15 @@ hipError_t launch_attention(int dtype, const void* q, const void* k, const void*
                        static_cast<const float*>(k), static_cast<const float*>(v), idx, cnt,
                        static_cast<float*>(out), lse, a);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_attention_merge(const float* part_o, const float* part_ml, void* out,
+                                  float* lse, const MergeArgs& a, hipStream_t s) {
+  const int64_t groups = (int64_t)a.n_split * a.nb;
+  if (groups == 0) return hipSuccess;
+  hipLaunchKernelGGL(attn_merge_kernel, dim3((unsigned)groups), dim3(64), 0, s, part_o, part_ml,
+                     static_cast<uint16_t*>(out), lse, a);
   return hipGetLastError();
 }
 

@@ -65,6 +65,17 @@ struct GlobalArgs {
   int32_t topk[kMaxHeads];
 };
 
+// Key-range split of long lists: a list head whose list can hold
+// kSplitMinBlocks or more key blocks runs as kSplitChunks work items per
+// query block, item c walking the list entries in key blocks
+// [c nb / C, (c + 1) nb / C). The waves that run together on an XCD then
+// read K and V from one key range instead of the head's whole extent. Each
+// item writes its unnormalised output and softmax statistics to a workspace
+// and a merge launch combines the chunks in a fixed order.
+constexpr int kSplitMinBlocks = 384;
+constexpr int kSplitChunks = 4;
+constexpr int64_t kSplitItemBytes = (int64_t)kBlock * kHeadDim * 4 + (int64_t)kBlock * 2 * 4;
+
 struct AttnArgs {
   int64_t n;
   int32_t nb;
@@ -72,10 +83,24 @@ struct AttnArgs {
   int32_t heads;          // heads in this launch (entries of order[])
   int32_t slab;           // query blocks of one head handled by one XCD: ceil(nb / 8)
   int32_t mode;           // 0: lists or dense per head; 1: every head dense; 2: STRIDE heads
+  int32_t splits;         // key ranges of a split head (kSplitChunks)
   float scale_log2;       // log2(e) / sqrt(64)
-  int16_t order[kMaxHeads];   // heads of this launch, most expensive first
+  float* part_o;          // split items' O^T accumulators, 64 x 64 fp32 each
+  float* part_ml;         // split items' (running max, row sum) per query
+  int16_t order[kMaxHeads];        // heads of this launch, longest work item first
+  int16_t split_pos[kMaxHeads];    // by order position: index among split heads, or -1
+  int32_t unit_start[kMaxHeads + 1];  // by order position: first work unit (slab units)
   int8_t dense[kMaxHeads];    // by head index: 1 = iterate all key blocks
   int32_t stride[kMaxHeads];  // by head index: key stride of a STRIDE head
+};
+
+// The merge of split heads: one wave per (split head, query block).
+struct MergeArgs {
+  int64_t n;
+  int32_t nb;
+  int32_t splits;
+  int32_t n_split;
+  int16_t head[kMaxHeads];  // by split index: head
 };
 
 // Block-wise DINO Top-K on caller-supplied per-token features.
@@ -105,6 +130,8 @@ hipError_t launch_nmse(int dtype, const void* ref, const void* test, void* works
 hipError_t launch_attention(int dtype, const void* q, const void* k, const void* v,
                             const int32_t* idx, const int32_t* cnt, void* out, float* lse,
                             const AttnArgs& a, hipStream_t s);
+hipError_t launch_attention_merge(const float* part_o, const float* part_ml, void* out,
+                                  float* lse, const MergeArgs& a, hipStream_t s);
 
 // Bytes of LDS the Top-K selection kernel needs for `rows` query blocks.
 size_t topk_lds_bytes(int rows, int nb);

@@ -43,10 +43,21 @@ def select_workspace(P, table, w, heads=None):
     return torch.empty(max(nbytes, 16) // 4, dtype=torch.int32, device="cuda")
 
 
+def attention_workspace(P, table, w):
+    """A device workspace with which the attention splits its long lists
+    into key ranges (16 bytes when no head qualifies)."""
+    import torch
+
+    code = P.BF16 if w.dtype == "bf16" else P.F32
+    nbytes = P.attention_workspace_bytes(table, w.frames, w.tokens_per_frame, code)
+    return torch.empty(max(nbytes, 16) // 4, dtype=torch.int32, device="cuda")
+
+
 def gpu_layer(P, w, q, k, v, table, want_scores=False, want_lse=True, workspace=True):
     """Runs estimate -> select -> attend through the binding; returns numpy
-    results. `workspace`: the two-launch Top-K selection (as bench.py runs
-    it) or, when False, the single-launch one."""
+    results. `workspace`: the two-launch Top-K selection and the attention
+    that splits long lists into key ranges (as bench.py runs them) or, when
+    False, the single-launch selection and unsplit attention."""
     import torch
 
     tq, tk, tv = (to_device(x, w.dtype) for x in (q, k, v))
@@ -55,8 +66,10 @@ def gpu_layer(P, w, q, k, v, table, want_scores=False, want_lse=True, workspace=
     ws = select_workspace(P, table, w) if workspace else None
     idx, cnt, scores = P.select_blocks(qp, kp, table, w.frames, w.tokens_per_frame,
                                        want_scores=want_scores, dtype=code, workspace=ws)
+    del ws
+    aws = attention_workspace(P, table, w) if workspace else None
     out, lse = P.sparse_attention(tq, tk, tv, table, w.frames, w.tokens_per_frame, idx, cnt,
-                                  want_lse=want_lse)
+                                  want_lse=want_lse, workspace=aws)
     torch.cuda.synchronize()
     res = {
         "q_pooled": qp.cpu().numpy(), "k_pooled": kp.transpose(1, 2).cpu().numpy(),
@@ -107,5 +120,5 @@ def finite(x):
     return bool(np.all(np.isfinite(x)))
 
 
-__all__ = ["NEAR_TIE", "TOL_BF16", "TOL_F32", "gpu_layer", "check_lists", "max_abs",
+__all__ = ["NEAR_TIE", "TOL_BF16", "TOL_F32", "gpu_layer", "attention_workspace", "check_lists", "max_abs",
            "sample_blocks", "to_device", "out_to_numpy", "gpu_list", "math"]

@@ -104,7 +104,7 @@ def test_new_classes_validation_and_capacity(B):
     fake = ctypes.c_void_p(0x1000)
     t = B.head_table([(B.STRIDE, 4), (0, 0)])
     assert lib.saf3r_sparse_attention(ctypes.byref(p), t, fake, fake, fake, None, None, 0,
-                                      None, None, None) == -1  # out missing, lists not required
+                                      None, None, None, 0, None) == -1  # out missing, lists not required
 
 
 def test_calls_reject_bad_arguments_before_launch(B):
@@ -127,12 +127,38 @@ def test_calls_reject_bad_arguments_before_launch(B):
     assert sel(ctypes.byref(p), t, fake, fake, fake, fake, 8, None, fake, need - 16, None) == -3
     assert sel(ctypes.byref(p), t, fake, fake, fake, fake, 8, None, fake, -1, None) == -1
     assert lib.saf3r_sparse_attention(ctypes.byref(p), t, fake, fake, fake, fake, fake, 4,
-                                      None, None, None) == -1
+                                      None, None, None, 0, None) == -1
     assert lib.saf3r_sparse_attention(ctypes.byref(p), t, fake, fake, fake, None, fake, 4,
-                                      fake, None, None) == -1
+                                      fake, None, None, 0, None) == -1
     assert lib.saf3r_sparse_attention(ctypes.byref(p), t, fake, fake, fake, fake, fake, 1,
-                                      fake, None, None) == -3
+                                      fake, None, None, 0, None) == -3
 
+
+def test_attention_workspace_bytes_and_validation(B):
+    """Split of long lists (Sec. 4.1 attention over kept blocks): bf16 list
+    heads that can keep 384 or more key blocks take 4 x nb items of
+    64 x 64 fp32 accumulators plus 64 (max, sum) pairs each."""
+    lib = B.load()
+    size = lib.saf3r_attention_workspace_bytes
+    item = 64 * 64 * 4 + 64 * 2 * 4
+    p = _p(B, heads=4, frames=64, T=1024)  # nb = 1024, 16 blocks per frame
+    t = B.head_table([(B.TOPK, 384), (B.TOPK, 383), (B.FRAME_LOCAL, 0), (B.DENSE, 0)])
+    assert size(ctypes.byref(p), t) == 1 * 4 * 1024 * item
+    both = B.head_table([(B.TOPK, 600), (B.GLOBAL_PROBE, 384), (B.COSINE_TOPK, 6), (B.STRIDE, 2)])
+    assert size(ctypes.byref(p), both) == 3 * 4 * 1024 * item  # cosine: 6 x 64 frames = 384
+    small = B.head_table([(B.COSINE_TOPK, 5), (B.ANCHOR, 0), (B.SKIP, 0), (B.DENSE, 0)])
+    assert size(ctypes.byref(p), small) == 0
+    assert size(ctypes.byref(_p(B, heads=4, frames=64, T=1024, dtype=B.F32)), t) == 0
+    assert size(None, t) == -1
+    fake = ctypes.c_void_p(0x1000)
+    need = 4 * 1024 * item
+    att = lib.saf3r_sparse_attention
+    assert att(ctypes.byref(p), t, fake, fake, fake, fake, fake, 384, fake, None,
+               fake, need - 1, None) == -3
+    assert att(ctypes.byref(p), t, fake, fake, fake, fake, fake, 384, fake, None,
+               ctypes.c_void_p(0x1008), need, None) == -1
+    assert att(ctypes.byref(p), t, fake, fake, fake, fake, fake, 383, fake, None,
+               fake, need, None) == -3  # cap below the table's capacity fails first
 
 def test_status_strings(B):
     lib = B.load()
@@ -192,4 +218,4 @@ def test_skip_heads_are_accepted_and_need_nothing(B):
     # a table of SKIP and DENSE heads needs no lists: a missing output fails first
     t = B.head_table([(B.SKIP, 0), (0, 0), (B.SKIP, 0)])
     assert lib.saf3r_sparse_attention(ctypes.byref(p), t, fake, fake, fake, None, None, 0,
-                                      None, None, None) == -1
+                                      None, None, None, 0, None) == -1

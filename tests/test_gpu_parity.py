@@ -173,6 +173,111 @@ def test_select_paths_agree(gpu_lib, name, layer):
             assert np.array_equal(sc.view(np.uint64), runs[0][2].view(np.uint64))
 
 
+def test_split_attention_paths_agree(gpu_lib):
+    """Top-K lists of 578 key blocks (of 4294) on the 274800-token layer run
+    split into four key ranges (with a workspace) and unsplit (without). Each
+    path is within the bf16 bounds of the exact result, rounding P to bf16
+    against different running maxima, so the two agree within twice those
+    bounds; and the split launch is deterministic. The split path's parity
+    against the oracle is checked by the sampled S200 tests, which run it."""
+    import torch
+
+    import paper_2607_03612_amd as P
+
+    w = WORKLOADS["S200xT1374-bf16-L24"]
+    layer = 3
+    q, k, v = make_qkv(w, layer=layer)
+    table = make_table(w, layer=layer)
+    assert max(t for p, t in table if p == O.TOPK) >= 512
+    S, T = w.frames, w.tokens_per_frame
+    tq, tk, tv = (PT.to_device(x, "bf16") for x in (q, k, v))
+    del q, k, v
+    qp, kp = P.estimate_blocks(tq, tk, table, S, T)
+    idx, cnt, _ = P.select_blocks(qp, kp, table, S, T, workspace=PT.select_workspace(P, table, w))
+    ws = PT.attention_workspace(P, table, w)
+    assert P.attention_workspace_bytes(table, S, T) > 0
+    print(f"[parity] split vs unsplit {w.name} layer {layer} table={table}", flush=True)
+    base, base_lse = P.sparse_attention(tq, tk, tv, table, S, T, idx, cnt, want_lse=True)
+    runs = [P.sparse_attention(tq, tk, tv, table, S, T, idx, cnt, want_lse=True, workspace=ws)
+            for _ in range(2)]
+    torch.cuda.synchronize()
+    for a, b in zip(runs[0], runs[1]):
+        assert torch.equal(a, b), "split launch not deterministic"
+    out, lse = runs[0]
+    err = float((out.float() - base.float()).abs().max())
+    lerr = float((lse - base_lse).abs().max())
+    print(f"[parity] split vs unsplit: out {err:.3e}, lse {lerr:.3e}", flush=True)
+    assert err <= 2 * PT.TOL_BF16 and lerr <= 2 * PT.LSE_TOL_BF16
+
+
+def test_split_attention_custom_lists(gpu_lib):
+    """Split attention on caller lists that exercise its cases: rows that
+    reach only the first two key ranges (empty items), one-block rows, the
+    partial last block, an empty row (zero output, LSE -inf) and lists of
+    every length. Sampled rows against the oracle, every row against the
+    unsplit launch."""
+    import torch
+
+    import paper_2607_03612_amd as P
+
+    w = Workload("split-8x8190", 8, 8190, "bf16", ("fixed", 0, 0, 50), heads=2)
+    nb, n = w.nb, w.tokens
+    assert nb == 1024 and n % 64 == 48
+    table = [(O.TOPK, 512), (O.TOPK, 600)]
+    cap = 600
+    q, k, v = make_qkv(w)
+    g = np.random.default_rng(3)
+    idx = np.full((2, nb, cap), -1, np.int32)
+    cnt = np.zeros((2, nb), np.int32)
+    for h in range(2):
+        for i in range(nb):
+            if h == 0 and i % 2 == 0:
+                lst = np.arange(512)  # key ranges 2 and 3 empty
+            elif h == 0 and i % 4 == 1:
+                lst = np.sort(g.choice(nb, size=int(g.integers(1, 513)), replace=False))
+            else:
+                lst = np.sort(g.choice(nb, size=int(g.integers(1, cap + 1)), replace=False))
+            idx[h, i, :len(lst)] = lst
+            cnt[h, i] = len(lst)
+    special = {(0, 5): [], (0, 7): [nb - 1], (1, 9): [0], (1, 11): list(range(800, 1024)),
+               (1, 13): [255, 256, 511, 512, 767, 768, nb - 1]}
+    for (h, i), lst in special.items():
+        idx[h, i] = -1
+        idx[h, i, :len(lst)] = lst
+        cnt[h, i] = len(lst)
+    tq, tk, tv = (PT.to_device(x, "bf16") for x in (q, k, v))
+    ti, tc = torch.from_numpy(idx).cuda(), torch.from_numpy(cnt).cuda()
+    ws = PT.attention_workspace(P, table, w)
+    assert P.attention_workspace_bytes(table, w.frames, w.tokens_per_frame) == 2 * 4 * nb * 16896
+    out, lse = P.sparse_attention(tq, tk, tv, table, w.frames, w.tokens_per_frame, ti, tc,
+                                  want_lse=True, workspace=ws)
+    base, base_lse = P.sparse_attention(tq, tk, tv, table, w.frames, w.tokens_per_frame, ti, tc,
+                                        want_lse=True)
+    torch.cuda.synchronize()
+    out_h, lse_h = PT.out_to_numpy(out), lse.cpu().numpy().astype(np.float64)
+    base_h, base_lse_h = PT.out_to_numpy(base), base_lse.cpu().numpy().astype(np.float64)
+    # the empty row: zero output and LSE -inf on both paths
+    r5 = O.block_range(5, n, 64)
+    assert np.all(out_h[0][r5.start:r5.stop] == 0) and np.all(np.isneginf(lse_h[0][r5.start:r5.stop]))
+    assert np.all(np.isneginf(base_lse_h[0][r5.start:r5.stop]))
+    fin = np.isfinite(base_lse_h)
+    assert np.array_equal(fin, np.isfinite(lse_h))
+    assert PT.max_abs(out_h, base_h) <= 2 * PT.TOL_BF16  # both within the bound of the exact result
+    assert PT.max_abs(lse_h[fin], base_lse_h[fin]) <= 2 * PT.LSE_TOL_BF16
+    rows = sorted(set(PT.sample_blocks(nb, 16, 4)) | {0, 1, 2, 3, 7, 9, 11, 13})
+    for h in range(2):
+        qh, kh, vh = (O.to_f64(x[h], "bf16") for x in (q, k, v))
+        for i in rows:
+            if cnt[h, i] == 0:  # the empty row, checked above
+                continue
+            r = O.block_range(i, n, 64)
+            ref, ref_lse = O.attend_block(qh, kh, vh, i, idx[h, i, :cnt[h, i]], 64)
+            err = PT.max_abs(out_h[h][r.start:r.stop], ref)
+            assert err <= PT.TOL_BF16, f"head {h} block {i}: max abs error {err}"
+            lerr = PT.max_abs(lse_h[h][r.start:r.stop], ref_lse)
+            assert lerr <= PT.LSE_TOL_BF16, f"head {h} block {i}: lse error {lerr}"
+
+
 # ------------------------------------------------------------ edge cases
 
 EDGE = [
