@@ -236,7 +236,7 @@ template <int MAXK>
 __device__ inline void select_row(RowKeys<MAXK>& row, uint32_t* lrow, int32_t* dst,
                                   int32_t* cnt_row, const double* qp_head, const double* kT,
                                   int i0, int r, int k, int nb, int cap, int lane) {
-  constexpr int kMaskWords = MAXK > 0 ? 1 : 4;  // C <= 48, or <= 256 (nb <= 16384)
+  constexpr int kMaskWords = MAXK > 0 ? (MAXK + 63) / 64 : 4;  // C <= MAXK, or <= 256 (nb <= 16384)
   const int C = row.C;
 
   // Kept: hi > T, plus `need` of the hi == T bucket (the best by stage 2),
@@ -869,6 +869,7 @@ hipError_t launch_select_topk_ws(const double* qp, const double* kpT, uint32_t* 
   if (chunks <= 4) return go(topk_rows_kernel<4>);
   if (chunks <= 16) return go(topk_rows_kernel<16>);
   if (chunks <= 48) return go(topk_rows_kernel<48>);
+  if (chunks <= 72) return go(topk_rows_kernel<72>);
   return go(topk_rows_kernel<0>);
 }
 

@@ -467,6 +467,31 @@ def test_equal_scores_keep_the_lowest_block_indices(gpu_lib):
         np.testing.assert_array_equal(res["idx"][h, :, :kk], np.tile(np.arange(kk), (w.nb, 1)))
 
 
+def test_equal_scores_long_rows(gpu_lib):
+    """The same tie rule where each lane of the selection owns 68 key blocks
+    (nb = 4200): the two-launch selection holds such rows in registers and
+    the single launch reads them from LDS; both must keep the lowest block
+    indices, through the tie refinement over bucket members in every slot."""
+    import torch
+
+    import paper_2607_03612_amd as P
+
+    w = Workload("ties-2x134400", 2, 134400, "bf16", ("fixed", 0, 0, 50), heads=2)
+    assert w.nb == 4200
+    q, k, _ = make_qkv(w)
+    k[:] = k[0, 0]
+    table = [(O.TOPK, 7), (O.TOPK, w.nb - 1)]
+    tq, tk = (PT.to_device(x, "bf16") for x in (q, k))
+    qp, kp = P.estimate_blocks(tq, tk, table, w.frames, w.tokens_per_frame)
+    for ws in (PT.select_workspace(P, table, w), None):
+        idx, cnt, _ = P.select_blocks(qp, kp, table, w.frames, w.tokens_per_frame, workspace=ws)
+        torch.cuda.synchronize()
+        idx, cnt = idx.cpu().numpy(), cnt.cpu().numpy()
+        for h, kk in enumerate((7, w.nb - 1)):
+            assert np.all(cnt[h] == kk), (h, ws is None)
+            np.testing.assert_array_equal(idx[h, :, :kk], np.tile(np.arange(kk), (w.nb, 1)))
+
+
 @pytest.mark.parametrize("stride", [8, 33])
 def test_stride_sampled_parity_large(gpu_lib, stride):
     """The 137400-token layer with STRIDE heads, checked on sampled query
