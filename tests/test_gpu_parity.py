@@ -110,6 +110,67 @@ def test_sampled_parity_large(gpu_lib, name, layer):
     _sampled_check(P, WORKLOADS[name], layer, samples=24, seed=layer + 1)
 
 
+def test_stack_layers_in_sequence(gpu_lib):
+    """Two layers of the 24-layer stack run back to back as bench.py runs the
+    stack: one index buffer sized for the larger capacity and viewed per
+    layer, one selection workspace and one attention workspace shared by
+    both, the earlier layer's lists overwritten by the later one's. Layer 8
+    (Top-K k = 125, not split) then layer 5 (k = 959, split, one dense head);
+    sampled rows of both against the oracle."""
+    import torch
+
+    import paper_2607_03612_amd as P
+
+    w = WORKLOADS["S200xT1374-bf16-L24"]
+    S, T, H, nb, n = w.frames, w.tokens_per_frame, w.heads, w.nb, w.tokens
+    layers = []
+    for layer in (8, 5):
+        q, k, v = make_qkv(w, layer=layer)
+        table = make_table(w, layer=layer)
+        layers.append((layer, q, k, v, table, P.index_capacity(table, S, T)))
+    idx_buf = torch.empty(H * nb * max(x[5] for x in layers), dtype=torch.int32, device="cuda")
+    cnt = torch.empty((H, nb), dtype=torch.int32, device="cuda")
+    sel_ws = torch.empty(max(P.select_workspace_bytes(x[4], S, T) for x in layers) // 4,
+                         dtype=torch.int32, device="cuda")
+    att_ws = torch.empty(max(P.attention_workspace_bytes(x[4], S, T) for x in layers) // 4,
+                         dtype=torch.int32, device="cuda")
+    assert P.attention_workspace_bytes(layers[1][4], S, T) > 0 == P.attention_workspace_bytes(layers[0][4], S, T)
+    for layer, q, k, v, table, cap in layers:
+        print(f"[parity] stack layer {layer} table={table}", flush=True)
+        tq, tk, tv = (PT.to_device(x, "bf16") for x in (q, k, v))
+        qp, kp = P.estimate_blocks(tq, tk, table, S, T)
+        idx = idx_buf[: H * nb * cap].view(H, nb, cap)
+        P.select_blocks(qp, kp, table, S, T, cap, idx, cnt, workspace=sel_ws)
+        out, lse = P.sparse_attention(tq, tk, tv, table, S, T, idx, cnt, want_lse=True,
+                                      workspace=att_ws)
+        torch.cuda.synchronize()
+        rows = PT.sample_blocks(nb, 6, layer)
+        idx_h, cnt_h = idx.cpu().numpy(), cnt.cpu().numpy()
+        for h, (pattern, topk) in enumerate(table):
+            spans = [O.block_range(i, n, 64) for i in rows]
+            got = [PT.out_to_numpy(out[h, r.start:r.stop]) for r in spans]
+            got_lse = [lse[h, r.start:r.stop].cpu().numpy().astype(np.float64) for r in spans]
+            qh, kh, vh = (O.to_f64(x[h], "bf16") for x in (q, k, v))
+            kbar = O.pool_blocks(kh, 64) if pattern == O.TOPK else None
+            for r_i, i in enumerate(rows):
+                r = O.block_range(i, n, 64)
+                if pattern == O.TOPK:
+                    lst, margin = O.topk_row(O.block_scores(O.pool_blocks(qh[r.start:r.stop], 64), kbar)[0], topk)
+                elif pattern == O.FRAME_LOCAL:
+                    lst, margin = O.frame_local_row(i, n, T, 64), np.inf
+                else:
+                    lst, margin = np.arange(nb), np.inf
+                if pattern != O.DENSE:
+                    c = int(cnt_h[h, i])
+                    if margin > PT.NEAR_TIE:
+                        assert np.array_equal(idx_h[h, i, :c], lst), (layer, h, i)
+                    lst = idx_h[h, i, :c]
+                ref, ref_lse = O.attend_block(qh, kh, vh, i, lst, 64)
+                assert PT.max_abs(got[r_i], ref) <= PT.TOL_BF16, (layer, h, i)
+                assert PT.max_abs(got_lse[r_i], ref_lse) <= PT.LSE_TOL_BF16, (layer, h, i)
+        del tq, tk, tv, out, lse
+
+
 def test_maximum_size_sampled(gpu_lib):
     """The largest problem the library accepts: N = 1048576 tokens (16384
     blocks) in 8 frames of 131072 tokens, two Top-K heads (k = 164) and one
