@@ -22,7 +22,15 @@
 //
 // Launch order: workgroup b runs on XCD b % 8; each XCD takes a contiguous
 // slab of query blocks of every head (neighbouring query blocks share kept
-// key blocks, which then hit in that XCD's L2), heads in decreasing cost.
+// key blocks, which then hit in that XCD's L2), longest work items first.
+//
+// Long lists can run split into key ranges: a work item is then (head, key
+// range c of splits, query block) and walks only its list's entries inside
+// range c, ranges in order within a head, so the waves that run together on
+// an XCD read K and V from one range rather than the head's whole extent.
+// Such an item stores its unnormalised O^T and (running max, row sum) per
+// query in a workspace; attn_merge_kernel combines the ranges of each query
+// block in range order.
 #include <type_traits>
 
 #include "saf3r_internal.h"
