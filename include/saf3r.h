@@ -203,7 +203,8 @@ int64_t saf3r_select_workspace_bytes(const saf3r_problem* problem, const saf3r_h
  *   lse_or_null  NULL, or device float32 [heads, N]
  *   workspace_or_null, workspace_bytes
  *                NULL: every query block of a head is one work item. A
- *                device buffer (16-byte aligned) of at least
+ *                device buffer (16-byte aligned, workspace_bytes >= 0, else
+ *                SAF3R_ERR_INVALID_ARGUMENT) of at least
  *                saf3r_attention_workspace_bytes(problem, table) bytes
  *                (else SAF3R_ERR_CAPACITY): bf16 list heads whose list can
  *                hold 384 or more key blocks run as 4 items per query block,

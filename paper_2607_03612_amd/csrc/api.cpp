@@ -321,8 +321,9 @@ saf3r_status saf3r_sparse_attention(const saf3r_problem* problem, const saf3r_he
   if (split_bytes < 0) return (saf3r_status)split_bytes;
   const bool split = workspace_or_null != nullptr && split_bytes > 0;
   if (workspace_or_null) {
+    if (workspace_bytes < 0 || reinterpret_cast<uintptr_t>(workspace_or_null) % 16 != 0)
+      return SAF3R_ERR_INVALID_ARGUMENT;
     if (workspace_bytes < split_bytes) return SAF3R_ERR_CAPACITY;
-    if (reinterpret_cast<uintptr_t>(workspace_or_null) % 16 != 0) return SAF3R_ERR_INVALID_ARGUMENT;
   }
 
   // Up to three launches: heads with block lists or dense (one kernel, work

@@ -157,6 +157,9 @@ def test_attention_workspace_bytes_and_validation(B):
                fake, need - 1, None) == -3
     assert att(ctypes.byref(p), t, fake, fake, fake, fake, fake, 384, fake, None,
                ctypes.c_void_p(0x1008), need, None) == -1
+    nosplit = B.head_table([(B.TOPK, 100), (B.FRAME_LOCAL, 0), (B.DENSE, 0), (B.DENSE, 0)])
+    assert att(ctypes.byref(p), nosplit, fake, fake, fake, fake, fake, 100, fake, None,
+               fake, -1, None) == -1  # a negative size is rejected even when nothing splits
     assert att(ctypes.byref(p), t, fake, fake, fake, fake, fake, 383, fake, None,
                fake, need, None) == -3  # cap below the table's capacity fails first
 
