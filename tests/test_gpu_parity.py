@@ -271,6 +271,43 @@ def test_split_attention_paths_agree(gpu_lib):
     assert err <= 2 * PT.TOL_BF16 and lerr <= 2 * PT.LSE_TOL_BF16
 
 
+def test_split_attention_with_global_probe_and_topk(gpu_lib):
+    """Split attention on lists the library selects: a Top-K head (k = 400)
+    and a global-probe head (k = 450) of 687 key blocks both qualify for the
+    key-range split, next to a frame-local and a dense head that do not;
+    sampled rows against the oracle's lists and attention."""
+    import paper_2607_03612_amd as P
+
+    w = WORKLOADS["S32xT1374-bf16"]
+    nb, n, T = w.nb, w.tokens, w.tokens_per_frame
+    q, k, v = make_qkv(w, heads=[0, 1, 2, 3])
+    table = [(O.TOPK, 400), (O.GLOBAL_PROBE, 450), (O.FRAME_LOCAL, 0), (O.DENSE, 0)]
+    assert P.attention_workspace_bytes(table, w.frames, T) == 2 * 4 * nb * 16896
+    res = PT.gpu_layer(P, w, q, k, v, table)
+    cap = res["idx"].shape[2]
+    rows = PT.sample_blocks(nb, 10, 21)
+    for h, (pattern, param) in enumerate(table):
+        qh, kh, vh = (O.to_f64(x[h], "bf16") for x in (q, k, v))
+        if pattern == O.GLOBAL_PROBE:
+            glist, gmargin, _ = O.global_probe_row(qh, kh, param, 64)
+        kbar = O.pool_blocks(kh, 64) if pattern == O.TOPK else None
+        for i in rows:
+            r = O.block_range(i, n, 64)
+            if pattern == O.TOPK:
+                lst, margin = O.topk_row(O.block_scores(O.pool_blocks(qh[r.start:r.stop], 64), kbar)[0], param)
+            elif pattern == O.GLOBAL_PROBE:
+                lst, margin = glist, gmargin
+            elif pattern == O.FRAME_LOCAL:
+                lst, margin = O.frame_local_row(i, n, T, 64), np.inf
+            else:
+                lst, margin = np.arange(nb), np.inf
+            if PT.check_lists(res, h, i, pattern, lst, margin, nb, cap) == "near_tie":
+                lst = PT.gpu_list(res, h, i)
+            ref, ref_lse = O.attend_block(qh, kh, vh, i, lst, 64)
+            assert PT.max_abs(res["out"][h][r.start:r.stop], ref) <= PT.TOL_BF16, (h, i)
+            assert PT.max_abs(res["lse"][h][r.start:r.stop], ref_lse) <= PT.LSE_TOL_BF16, (h, i)
+
+
 def test_split_attention_custom_lists(gpu_lib):
     """Split attention on caller lists that exercise its cases: rows that
     reach only the first two key ranges (empty items), one-block rows, the
