@@ -140,9 +140,9 @@ def topk_row(scores_row: np.ndarray, k: int):
 
 
 def anchor_row(anchor: int, n: int, tokens_per_frame: int, block: int) -> np.ndarray:
-    """Key blocks of the anchor frame (static kernel, Sec. 4.1: every query
-    attends to a designated anchor frame): the blocks that hold a token of
-    frame ``anchor``. The same for every query block."""
+    """Key blocks of the anchor frame (static kernel, Sec. 4.1: all queries
+    look at one chosen frame): the blocks that hold a token of frame
+    ``anchor``. The same for every query block."""
     token_frame = np.arange(n) // tokens_per_frame
     token_block = np.arange(n) // block
     return np.unique(token_block[token_frame == anchor]).astype(np.int64)
