@@ -222,3 +222,18 @@ def test_skip_heads_are_accepted_and_need_nothing(B):
     t = B.head_table([(B.SKIP, 0), (0, 0), (B.SKIP, 0)])
     assert lib.saf3r_sparse_attention(ctypes.byref(p), t, fake, fake, fake, None, None, 0,
                                       None, None, None, 0, None) == -1
+
+
+def test_missing_library_fails_loudly(B, tmp_path, monkeypatch):
+    """Without the built library every entry of the binding raises; nothing
+    falls back to another implementation."""
+    monkeypatch.setattr(B, "_LIB", None)
+    missing = str(tmp_path / "libsaf3r.so")
+    with pytest.raises(RuntimeError, match="missing"):
+        B.load(missing)
+    monkeypatch.setattr(B, "LIB_PATH", missing)
+    monkeypatch.setattr(B.load, "__defaults__", (missing,))
+    with pytest.raises(RuntimeError, match="missing"):
+        B.index_capacity([(B.TOPK, 4)], 2, 100)
+    with pytest.raises(RuntimeError, match="missing"):
+        B.attention_workspace_bytes([(B.TOPK, 4)], 2, 100)
