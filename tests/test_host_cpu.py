@@ -48,3 +48,17 @@ def test_choice_matches_progressive_substitution():
         got = profiler.choose(errors, costs)
         want = [O.progressive_substitution(errors[:, h], costs[:, h]) for h in range(H)]
         assert got == want
+
+
+def test_bench_refuses_more_than_one_gpu():
+    """bench.py runs on one GPU; asking for more exits with status 2 and says
+    so, before anything touches a GPU."""
+    import subprocess
+    import sys
+    from pathlib import Path
+
+    root = Path(__file__).resolve().parents[1]
+    r = subprocess.run([sys.executable, str(root / "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr and r.stdout == ""
