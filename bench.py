@@ -28,6 +28,7 @@ sys.path.insert(0, ROOT)
 METRIC = "ms per global-attn layer + dense-equiv TFLOP/s at S=100×1374 tok, 16 heads"
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_F32_TFLOPS = 157.3     # MI355X fp32 matrix
+PEAK_F64_TFLOPS = 78.6      # MI355X fp64 (matrix and vector)
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_traffic.json")
 
@@ -579,6 +580,15 @@ def main():
             "achieved": round(est_bytes / (est_cold_ms * 1e-3) / 1e9, 1), "peak": PEAK_HBM_GBS,
             "unit": "GB/s", "frac": round(est_bytes / (est_cold_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
             "stream_read_reference_GBps": round(est_bytes / (ref_cold_ms * 1e-3) / 1e9, 1),
+        },
+        "select_roofline": {
+            # Top-K scores of every (query block, key block) pair in float64
+            # on the matrix cores: 2 * nb^2 * 64 FLOP per Top-K head
+            "kernel": "topk_score_kernel + topk_rows_kernel", "bound": "mfma-fp64",
+            "flop_per_launch": 2 * nb * nb * 64 * n_topk, "launch_ms": round(sel_ms, 4),
+            "achieved": round(2 * nb * nb * 64 * n_topk / (sel_ms * 1e-3) / 1e12, 2),
+            "peak": PEAK_F64_TFLOPS, "unit": "TFLOP/s",
+            "frac": round(2 * nb * nb * 64 * n_topk / (sel_ms * 1e-3) / 1e12 / PEAK_F64_TFLOPS, 4),
         },
         "dense_baseline": dense,
         "next_rows": next_rows,
