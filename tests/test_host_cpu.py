@@ -62,3 +62,47 @@ def test_bench_refuses_more_than_one_gpu():
                        capture_output=True, text=True, timeout=120)
     assert r.returncode == 2
     assert "one GPU" in r.stderr and r.stdout == ""
+
+
+def _list_len(pattern, param, n, T, nb):
+    """Longest list of a head's class, from the oracle's own definitions."""
+    if pattern == B.FRAME_LOCAL:
+        return max(len(O.frame_local_row(i, n, T, 64)) for i in range(nb))
+    if pattern == B.ANCHOR:
+        return len(O.anchor_row(param, n, T, 64))
+    if pattern == B.COSINE_TOPK:
+        sim = np.random.default_rng(0).standard_normal(nb)
+        return len(O.cosine_topk_row(sim, param, T, 64)[0])
+    return param  # TOPK, GLOBAL_PROBE
+
+
+@pytest.mark.parametrize("frames,T", [(2, 25000), (64, 400), (8, 5000), (40, 700), (3, 13000)])
+def test_capacity_and_attention_split_match_oracle_lists(frames, T):
+    """The library's index capacity (longest list over list heads) and the
+    attention split (bf16 list heads whose lists can hold 384 or more key
+    blocks, 4 key ranges of nb items each) against list lengths from the
+    oracle's class definitions, on seeded random tables."""
+    import ctypes
+
+    lib = B.load()
+    n = frames * T
+    nb = -(-n // 64)
+    g = np.random.default_rng(frames * 100003 + T)
+    classes = [B.DENSE, B.FRAME_LOCAL, B.TOPK, B.ANCHOR, B.STRIDE, B.GLOBAL_PROBE, B.COSINE_TOPK, B.SKIP]
+    for trial in range(12):
+        table = []
+        for _ in range(8):
+            c = int(g.choice(classes))
+            param = {B.TOPK: int(g.integers(1, nb + 1)), B.GLOBAL_PROBE: int(g.integers(1, nb + 1)),
+                     B.ANCHOR: int(g.integers(0, frames)), B.STRIDE: int(g.integers(1, n + 1)),
+                     B.COSINE_TOPK: int(g.integers(1, 65))}.get(c, 0)
+            table.append((c, param))
+        listed = [(c, p) for c, p in table if c in (B.FRAME_LOCAL, B.TOPK, B.ANCHOR, B.GLOBAL_PROBE,
+                                                   B.COSINE_TOPK)]
+        lens = [_list_len(c, p, n, T, nb) for c, p in listed]
+        for dtype in (B.BF16, B.F32):
+            p = B.problem(len(table), frames, T, dtype)
+            t = B.head_table(table)
+            assert lib.saf3r_index_capacity(ctypes.byref(p), t) == max(lens + [1]), (table, lens)
+            want = 4 * nb * 16896 * sum(1 for x in lens if x >= 384) if dtype == B.BF16 else 0
+            assert lib.saf3r_attention_workspace_bytes(ctypes.byref(p), t) == want, (table, lens)
