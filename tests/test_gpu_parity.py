@@ -274,14 +274,15 @@ def test_split_attention_paths_agree(gpu_lib):
 def test_split_attention_with_global_probe_and_topk(gpu_lib):
     """Split attention on lists the library selects: a Top-K head (k = 400)
     and a global-probe head (k = 450) of 687 key blocks both qualify for the
-    key-range split, next to a frame-local and a dense head that do not;
-    sampled rows against the oracle's lists and attention."""
+    key-range split, next to a frame-local, a dense and a stride-9 head (its
+    own launch) that do not; sampled rows against the oracle's lists and
+    attention."""
     import paper_2607_03612_amd as P
 
     w = WORKLOADS["S32xT1374-bf16"]
     nb, n, T = w.nb, w.tokens, w.tokens_per_frame
-    q, k, v = make_qkv(w, heads=[0, 1, 2, 3])
-    table = [(O.TOPK, 400), (O.GLOBAL_PROBE, 450), (O.FRAME_LOCAL, 0), (O.DENSE, 0)]
+    q, k, v = make_qkv(w, heads=[0, 1, 2, 3, 4])
+    table = [(O.TOPK, 400), (O.GLOBAL_PROBE, 450), (O.FRAME_LOCAL, 0), (O.DENSE, 0), (O.STRIDE, 9)]
     assert P.attention_workspace_bytes(table, w.frames, T) == 2 * 4 * nb * 16896
     res = PT.gpu_layer(P, w, q, k, v, table)
     cap = res["idx"].shape[2]
@@ -299,6 +300,12 @@ def test_split_attention_with_global_probe_and_topk(gpu_lib):
                 lst, margin = glist, gmargin
             elif pattern == O.FRAME_LOCAL:
                 lst, margin = O.frame_local_row(i, n, T, 64), np.inf
+            elif pattern == O.STRIDE:
+                assert res["cnt"][h, i] == _stride_blocks(n, param)
+                ref, ref_lse = O.attend_tokens(qh, kh, vh, r, O.stride_keys(n, param))
+                assert PT.max_abs(res["out"][h][r.start:r.stop], ref) <= PT.TOL_BF16, (h, i)
+                assert PT.max_abs(res["lse"][h][r.start:r.stop], ref_lse) <= PT.LSE_TOL_BF16, (h, i)
+                continue
             else:
                 lst, margin = np.arange(nb), np.inf
             if PT.check_lists(res, h, i, pattern, lst, margin, nb, cap) == "near_tie":
