@@ -61,7 +61,8 @@ def source_sha(path):
 
 
 def recorded_traffic(workload):
-    """HBM bytes per attention launch from the committed rocprofv3 counter
+    """HBM bytes per attention launch (for the 24-layer stack, the sum over
+    the attention launches of one pass) from the committed rocprofv3 counter
     runs, if they were taken on the current kernel source."""
     try:
         rec = json.load(open(TRAFFIC_FILE))
@@ -338,7 +339,9 @@ def run_stack(args, P, torch, w):
         "roofline": {
             "kernel": "attn_bf16_kernel" if w.dtype == "bf16" else "attn_f32_kernel",
             "bound": "mfma", "achieved": round(att_tflops, 2), "peak": peak, "unit": "TFLOP/s",
-            "frac": round(att_tflops / peak, 4), "traffic": None,
+            "frac": round(att_tflops / peak, 4),
+            # FETCH_SIZE + WRITE_SIZE of the 24 attention launches of one pass
+            "traffic": recorded_traffic(w.name),
             "flop_per_step": flop_total, "attention_ms_per_step": round(att_total, 4),
         },
         "kernels_ms_per_step": {"estimate": round(float(ph[0]), 4), "select": round(float(ph[1]), 4),
