@@ -274,13 +274,15 @@ static int attention_cost(const Shape& s, const saf3r_head_cfg* table, int h, in
   }
 }
 
-// A list head whose list can reach kSplitMinBlocks key blocks runs split
-// into key ranges (bf16 only).
+// On a layer of at least kSplitMinExtent key blocks, a list head whose list
+// can reach kSplitMinBlocks key blocks runs split into key ranges (bf16
+// only).
 static bool attention_split(const Shape& s, const saf3r_head_cfg* table, int h, int cost) {
   const int p = table[h].pattern;
   const bool listed = p == SAF3R_FRAME_LOCAL || p == SAF3R_TOPK || p == SAF3R_ANCHOR ||
                       p == SAF3R_GLOBAL_PROBE || p == SAF3R_COSINE_TOPK;
-  return listed && s.dtype == SAF3R_BF16 && cost >= saf3r::kSplitMinBlocks;
+  return listed && s.dtype == SAF3R_BF16 && s.nb >= saf3r::kSplitMinExtent &&
+         cost >= saf3r::kSplitMinBlocks;
 }
 
 int64_t saf3r_attention_workspace_bytes(const saf3r_problem* problem, const saf3r_head_cfg* table) {

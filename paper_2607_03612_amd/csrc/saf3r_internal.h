@@ -65,14 +65,15 @@ struct GlobalArgs {
   int32_t topk[kMaxHeads];
 };
 
-// Key-range split of long lists: a list head whose list can hold
-// kSplitMinBlocks or more key blocks runs as kSplitChunks work items per
-// query block, item c walking the list entries in key blocks
-// [c nb / C, (c + 1) nb / C). The waves that run together on an XCD then
+// Key-range split of long lists: on a layer of at least kSplitMinExtent key
+// blocks, a list head whose list can hold kSplitMinBlocks or more key blocks
+// runs as kSplitChunks work items per query block, item c walking the list
+// entries in key blocks [c nb / C, (c + 1) nb / C). The waves that run together on an XCD then
 // read K and V from one key range instead of the head's whole extent. Each
 // item writes its unnormalised output and softmax statistics to a workspace
 // and a merge launch combines the chunks in a fixed order.
 constexpr int kSplitMinBlocks = 384;
+constexpr int kSplitMinExtent = 4096;
 constexpr int kSplitChunks = 4;
 constexpr int64_t kSplitItemBytes = (int64_t)kBlock * kHeadDim * 4 + (int64_t)kBlock * 2 * 4;
 

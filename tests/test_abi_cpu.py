@@ -135,23 +135,26 @@ def test_calls_reject_bad_arguments_before_launch(B):
 
 
 def test_attention_workspace_bytes_and_validation(B):
-    """Split of long lists (Sec. 4.1 attention over kept blocks): bf16 list
-    heads that can keep 384 or more key blocks take 4 x nb items of
-    64 x 64 fp32 accumulators plus 64 (max, sum) pairs each."""
+    """Split of long lists (Sec. 4.1 attention over kept blocks): on layers
+    of 4096 or more key blocks, bf16 list heads that can keep 384 or more
+    key blocks take 4 x nb items of 64 x 64 fp32 accumulators plus 64
+    (max, sum) pairs each."""
     lib = B.load()
     size = lib.saf3r_attention_workspace_bytes
     item = 64 * 64 * 4 + 64 * 2 * 4
-    p = _p(B, heads=4, frames=64, T=1024)  # nb = 1024, 16 blocks per frame
+    p = _p(B, heads=4, frames=64, T=4096)  # nb = 4096, 64 blocks per frame
     t = B.head_table([(B.TOPK, 384), (B.TOPK, 383), (B.FRAME_LOCAL, 0), (B.DENSE, 0)])
-    assert size(ctypes.byref(p), t) == 1 * 4 * 1024 * item
+    assert size(ctypes.byref(p), t) == 1 * 4 * 4096 * item
     both = B.head_table([(B.TOPK, 600), (B.GLOBAL_PROBE, 384), (B.COSINE_TOPK, 6), (B.STRIDE, 2)])
-    assert size(ctypes.byref(p), both) == 3 * 4 * 1024 * item  # cosine: 6 x 64 frames = 384
+    assert size(ctypes.byref(p), both) == 3 * 4 * 4096 * item  # cosine: 6 x 64 frames = 384
     small = B.head_table([(B.COSINE_TOPK, 5), (B.ANCHOR, 0), (B.SKIP, 0), (B.DENSE, 0)])
     assert size(ctypes.byref(p), small) == 0
-    assert size(ctypes.byref(_p(B, heads=4, frames=64, T=1024, dtype=B.F32)), t) == 0
+    assert size(ctypes.byref(_p(B, heads=4, frames=64, T=4096, dtype=B.F32)), t) == 0
+    # a shorter layer (nb = 4095) splits nothing, whatever the lists
+    assert size(ctypes.byref(_p(B, heads=4, frames=63, T=4160)), both) == 0
     assert size(None, t) == -1
     fake = ctypes.c_void_p(0x1000)
-    need = 4 * 1024 * item
+    need = 4 * 4096 * item
     att = lib.saf3r_sparse_attention
     assert att(ctypes.byref(p), t, fake, fake, fake, fake, fake, 384, fake, None,
                fake, need - 1, None) == -3

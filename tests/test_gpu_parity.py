@@ -273,20 +273,20 @@ def test_split_attention_paths_agree(gpu_lib):
 
 def test_split_attention_with_global_probe_and_topk(gpu_lib):
     """Split attention on lists the library selects: a Top-K head (k = 400)
-    and a global-probe head (k = 450) of 687 key blocks both qualify for the
-    key-range split, next to a frame-local, a dense and a stride-9 head (its
+    and a global-probe head (k = 450) of 4294 key blocks both qualify for
+    the key-range split, next to a frame-local, a dense and a stride-9 head (its
     own launch) that do not; sampled rows against the oracle's lists and
     attention."""
     import paper_2607_03612_amd as P
 
-    w = WORKLOADS["S32xT1374-bf16"]
+    w = WORKLOADS["S200xT1374-bf16-L24"]
     nb, n, T = w.nb, w.tokens, w.tokens_per_frame
     q, k, v = make_qkv(w, heads=[0, 1, 2, 3, 4])
     table = [(O.TOPK, 400), (O.GLOBAL_PROBE, 450), (O.FRAME_LOCAL, 0), (O.DENSE, 0), (O.STRIDE, 9)]
     assert P.attention_workspace_bytes(table, w.frames, T) == 2 * 4 * nb * 16896
     res = PT.gpu_layer(P, w, q, k, v, table)
     cap = res["idx"].shape[2]
-    rows = PT.sample_blocks(nb, 10, 21)
+    rows = PT.sample_blocks(nb, 8, 21)
     for h, (pattern, param) in enumerate(table):
         qh, kh, vh = (O.to_f64(x[h], "bf16") for x in (q, k, v))
         if pattern == O.GLOBAL_PROBE:
@@ -317,17 +317,17 @@ def test_split_attention_with_global_probe_and_topk(gpu_lib):
 
 def test_split_attention_custom_lists(gpu_lib):
     """Split attention on caller lists that exercise its cases: rows that
-    reach only the first two key ranges (empty items), one-block rows, the
-    partial last block, an empty row (zero output, LSE -inf) and lists of
-    every length. Sampled rows against the oracle, every row against the
-    unsplit launch."""
+    reach only the first of the four key ranges (empty items), one-block
+    rows, lists on the range boundaries, the partial last block, an empty
+    row (zero output, LSE -inf) and lists of every length. Sampled rows
+    against the oracle, every row against the unsplit launch."""
     import torch
 
     import paper_2607_03612_amd as P
 
-    w = Workload("split-8x8190", 8, 8190, "bf16", ("fixed", 0, 0, 50), heads=2)
+    w = Workload("split-8x32766", 8, 32766, "bf16", ("fixed", 0, 0, 50), heads=2)
     nb, n = w.nb, w.tokens
-    assert nb == 1024 and n % 64 == 48
+    assert nb == 4096 and n % 64 == 48
     table = [(O.TOPK, 512), (O.TOPK, 600)]
     cap = 600
     q, k, v = make_qkv(w)
@@ -337,15 +337,15 @@ def test_split_attention_custom_lists(gpu_lib):
     for h in range(2):
         for i in range(nb):
             if h == 0 and i % 2 == 0:
-                lst = np.arange(512)  # key ranges 2 and 3 empty
+                lst = np.arange(0, 1024, 2)  # only the first of the four key ranges
             elif h == 0 and i % 4 == 1:
                 lst = np.sort(g.choice(nb, size=int(g.integers(1, 513)), replace=False))
             else:
                 lst = np.sort(g.choice(nb, size=int(g.integers(1, cap + 1)), replace=False))
             idx[h, i, :len(lst)] = lst
             cnt[h, i] = len(lst)
-    special = {(0, 5): [], (0, 7): [nb - 1], (1, 9): [0], (1, 11): list(range(800, 1024)),
-               (1, 13): [255, 256, 511, 512, 767, 768, nb - 1]}
+    special = {(0, 5): [], (0, 7): [nb - 1], (1, 9): [0], (1, 11): list(range(3200, 3424)),
+               (1, 13): [1023, 1024, 2047, 2048, 3071, 3072, nb - 1]}
     for (h, i), lst in special.items():
         idx[h, i] = -1
         idx[h, i, :len(lst)] = lst

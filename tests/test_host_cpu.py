@@ -67,7 +67,11 @@ def test_bench_refuses_more_than_one_gpu():
 def _list_len(pattern, param, n, T, nb):
     """Longest list of a head's class, from the oracle's own definitions."""
     if pattern == B.FRAME_LOCAL:
-        return max(len(O.frame_local_row(i, n, T, 64)) for i in range(nb))
+        # the longest list is a block's that holds a frame boundary (its list
+        # contains both frames' blocks, so every list of either frame), or the
+        # first block when there is one frame
+        rows = {0, nb - 1} | {min((f * T) // 64, nb - 1) for f in range(1, -(-n // T))}
+        return max(len(O.frame_local_row(i, n, T, 64)) for i in sorted(rows))
     if pattern == B.ANCHOR:
         return len(O.anchor_row(param, n, T, 64))
     if pattern == B.COSINE_TOPK:
@@ -76,12 +80,14 @@ def _list_len(pattern, param, n, T, nb):
     return param  # TOPK, GLOBAL_PROBE
 
 
-@pytest.mark.parametrize("frames,T", [(2, 25000), (64, 400), (8, 5000), (40, 700), (3, 13000)])
+@pytest.mark.parametrize("frames,T", [(2, 25000), (64, 400), (8, 5000), (40, 700), (3, 13000),
+                                     (2, 131072), (64, 4100)])
 def test_capacity_and_attention_split_match_oracle_lists(frames, T):
     """The library's index capacity (longest list over list heads) and the
-    attention split (bf16 list heads whose lists can hold 384 or more key
-    blocks, 4 key ranges of nb items each) against list lengths from the
-    oracle's class definitions, on seeded random tables."""
+    attention split (on layers of 4096 or more key blocks, bf16 list heads
+    whose lists can hold 384 or more key blocks, 4 key ranges of nb items
+    each) against list lengths from the oracle's class definitions, on
+    seeded random tables."""
     import ctypes
 
     lib = B.load()
@@ -104,5 +110,6 @@ def test_capacity_and_attention_split_match_oracle_lists(frames, T):
             p = B.problem(len(table), frames, T, dtype)
             t = B.head_table(table)
             assert lib.saf3r_index_capacity(ctypes.byref(p), t) == max(lens + [1]), (table, lens)
-            want = 4 * nb * 16896 * sum(1 for x in lens if x >= 384) if dtype == B.BF16 else 0
+            split = dtype == B.BF16 and nb >= 4096
+            want = 4 * nb * 16896 * sum(1 for x in lens if x >= 384) if split else 0
             assert lib.saf3r_attention_workspace_bytes(ctypes.byref(p), t) == want, (table, lens)
