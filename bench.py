@@ -365,7 +365,8 @@ def main():
     ap.add_argument("--next-rows", type=int, default=1,
                     help="also time the stride, global-probe, cosine and NMSE kernels (0 = skip)")
     ap.add_argument("--split", type=int, default=1, choices=(0, 1),
-                    help="1: pass the attention workspace, so lists of 384+ key blocks run split "
+                    help="1: pass the attention workspace, so lists of 384+ key blocks (on layers of 4096+ "
+                         "key blocks) run split "
                          "into key ranges; 0: the unsplit launch (same work and results)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run three device-to-device copies of MIB MiB (a plain copy "
@@ -429,7 +430,7 @@ def main():
     # single launch that keeps score rows in LDS; the same lists)
     sel_ws_bytes = P.select_workspace_bytes(table, S, T, code)
     sel_ws = torch.empty(max(sel_ws_bytes, 16) // 4, dtype=torch.int32, device=dev)
-    # long lists (384+ key blocks) run split into key ranges through a
+    # long lists (384+ key blocks, layers of 4096+) run split into key ranges through a
     # workspace; none at this layer's budget, the call takes it all the same
     att_ws_bytes = P.attention_workspace_bytes(table, S, T, code)
     att_ws = torch.empty(max(att_ws_bytes, 16) // 4, dtype=torch.int32, device=dev) if args.split else None
