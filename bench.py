@@ -75,17 +75,25 @@ def recorded_traffic(workload):
     return r.get("bytes_per_launch")
 
 
-def oracle_sample(w, q, k, v, table, rows_per_head, seed=0):
+def sample_rows(nb, rows_per_head, seed=0):
+    """The seeded query blocks the oracle sample covers (the same for every head)."""
+    return sorted(int(i) for i in np.random.default_rng(seed).choice(nb, size=min(rows_per_head, nb),
+                                                                     replace=False))
+
+
+def oracle_sample(w, q, k, v, table, rows_per_head, seed=0, results=None):
     """The fp64 oracle on a seeded sample of query blocks of every head.
 
     Per head, the full per-head work (widening to fp64, pooling every key
     block of a Top-K head) is timed once; the per-query-block work (probe,
     scores, selection, attention) is timed on the sample and scaled to all
-    query blocks. Returns (estimated seconds per layer, sampled rows per head)."""
+    query blocks. Returns (estimated seconds per layer, sampled rows per head);
+    with `results` (a dict), also keeps each sampled row's list, margin and
+    output under (head, block)."""
     import oracle as O
 
     nb, n, T = w.nb, w.tokens, w.tokens_per_frame
-    rows = sorted(np.random.default_rng(seed).choice(nb, size=min(rows_per_head, nb), replace=False))
+    rows = sample_rows(nb, rows_per_head, seed)
     est = 0.0
     for h, (pattern, topk) in enumerate(table):
         t0 = time.perf_counter()
@@ -96,15 +104,45 @@ def oracle_sample(w, q, k, v, table, rows_per_head, seed=0):
             r = O.block_range(i, n, 64)
             if pattern == O.TOPK:
                 qbar = O.pool_blocks(qh[r.start:r.stop], 64)
-                lst, _ = O.topk_row(O.block_scores(qbar, kbar)[0], topk)
+                lst, margin = O.topk_row(O.block_scores(qbar, kbar)[0], topk)
             elif pattern == O.FRAME_LOCAL:
-                lst = O.frame_local_row(i, n, T, 64)
+                lst, margin = O.frame_local_row(i, n, T, 64), None
             else:
-                lst = np.arange(nb)
-            O.attend_block(qh, kh, vh, i, lst, 64)
+                lst, margin = np.arange(nb), None
+            ref = O.attend_block(qh, kh, vh, i, lst, 64)
+            if results is not None:
+                results[(h, i)] = (lst, margin, ref[0])
         t2 = time.perf_counter()
         est += (t1 - t0) + (t2 - t1) * nb / len(rows)
     return est, len(rows)
+
+
+def parity_sample(res, sampled, out_sampled, idx_h, cnt_h, table, n, dtype):
+    """The timed step's lists and outputs on the oracle sample's query blocks
+    against the oracle: lists equal except where the oracle's Top-K margin is
+    at most 1e-6 (near-ties, counted), outputs within the dtype's bound."""
+    offset, pos = {}, 0
+    for i in sampled:
+        offset[i] = pos
+        pos += min(64, n - i * 64)
+    equal = near = mismatch = 0
+    err = 0.0
+    for (h, i), (lst, margin, ref) in res.items():
+        if table[h][0] != 0:  # dense heads carry no list
+            c = int(cnt_h[h, i])
+            if np.array_equal(idx_h[h, i, :c], lst):
+                equal += 1
+            elif margin is not None and margin <= 1e-6:
+                near += 1
+                continue
+            else:
+                mismatch += 1
+                continue
+        got = out_sampled[h, offset[i]:offset[i] + ref.shape[0]]
+        err = max(err, float(np.max(np.abs(got - ref))))
+    return {"query_blocks": len(res), "lists_equal": equal, "near_ties_differing": near,
+            "list_mismatches": mismatch, "max_abs_err": err,
+            "bound": 2e-2 if dtype == "bf16" else 1e-4}
 
 
 def blas_threads():
@@ -466,6 +504,12 @@ def main():
     att_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
 
     idx_h, cnt_h = idx.cpu().numpy(), cnt.cpu().numpy()
+    # the timed step's outputs on the query blocks the oracle sample covers
+    # (later launches below reuse `out`)
+    sampled = sample_rows(nb, args.cpu_rows, args.seed) if args.cpu_rows > 0 else []
+    tok = np.concatenate([np.arange(i * 64, min((i + 1) * 64, N)) for i in sampled]) if sampled else None
+    out_sampled = (out[:, torch.from_numpy(tok).to(dev)].float().cpu().numpy().astype(np.float64)
+                   if sampled else None)
     flops_kept = kept_flops(idx_h, cnt_h, table, N, nb)
     flops_dense = 4 * N * N * 64 * H
     kept_pairs = sum(nb * nb if p == 0 else int(cnt_h[h].sum()) for h, (p, _) in enumerate(table))
@@ -537,10 +581,14 @@ def main():
         log(f"[bench] next rows {next_rows}")
 
     cpu = None
+    parity = None
     if args.cpu_rows > 0:
         t0 = time.perf_counter()
-        sec, rows = oracle_sample(w, q, k, v, table, args.cpu_rows, seed=args.seed)
+        res = {}
+        sec, rows = oracle_sample(w, q, k, v, table, args.cpu_rows, seed=args.seed, results=res)
         wall = time.perf_counter() - t0
+        parity = parity_sample(res, sampled, out_sampled, idx_h, cnt_h, table, N, w.dtype)
+        log(f"[bench] parity on the oracle sample {parity}")
         cpu = {"value": round(flops_dense / sec / 1e12, 6), "unit": "dense-equiv TFLOP/s",
                "cores": blas_threads(), "kind": "oracle",
                "ms_per_layer": round(sec * 1e3, 1),
@@ -597,6 +645,7 @@ def main():
         "dense_baseline": dense,
         "next_rows": next_rows,
         "cpu_baseline": cpu,
+        "parity_sample": parity,
     }
     print(json.dumps(result), flush=True)
 
