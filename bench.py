@@ -292,9 +292,16 @@ def run_stack(args, P, torch, w):
             ev[3].record()
         return idx
 
-    # algorithmic FLOP and achieved sparsity of every layer, outside the timing
-    for x in layers:
+    # algorithmic FLOP and achieved sparsity of every layer, outside the timing;
+    # layer 0's lists and outputs on the oracle sample's query blocks
+    cpu_rows = min(args.cpu_rows, 16)
+    sampled = sample_rows(nb, cpu_rows, args.seed) if cpu_rows > 0 else []
+    for l, x in enumerate(layers):
         idx = run_layer(x)
+        if l == 0 and sampled:
+            tok = np.concatenate([np.arange(i * 64, min((i + 1) * 64, N)) for i in sampled])
+            out0 = out[:, torch.from_numpy(tok).to(dev)].float().cpu().numpy().astype(np.float64)
+            idx0, cnt0 = idx.cpu().numpy(), cnt.cpu().numpy()
         x["flop"] = kept_flops_device(torch, idx, cnt, x["table"], N, nb)
         c = cnt.to(torch.int64)
         x["pairs"] = sum(nb * nb if p == 0 else int(c[h].sum().item())
@@ -342,11 +349,15 @@ def run_stack(args, P, torch, w):
         f"attention {att_tflops:.1f} TFLOP/s")
 
     cpu = None
-    if args.cpu_rows > 0:
-        rows = min(args.cpu_rows, 16)
+    parity = None
+    if cpu_rows > 0:
         t0 = time.perf_counter()
-        sec, rows = oracle_sample(w, *host0, layers[0]["table"], rows, seed=args.seed)
+        res = {}
+        sec, rows = oracle_sample(w, *host0, layers[0]["table"], cpu_rows, seed=args.seed, results=res)
         wall = time.perf_counter() - t0
+        parity = parity_sample(res, sampled, out0, idx0, cnt0, layers[0]["table"], N, w.dtype)
+        parity["layer"] = 0
+        log(f"[stack] parity on the oracle sample {parity}")
         cpu = {"value": round(flops_dense / sec / 1e12, 6), "unit": "dense-equiv TFLOP/s",
                "cores": blas_threads(), "kind": "oracle",
                "ms_per_layer": round(sec * 1e3, 1),
@@ -386,6 +397,7 @@ def run_stack(args, P, torch, w):
                                 "attention": round(float(ph[2]), 4)},
         "per_layer": per_layer,
         "cpu_baseline": cpu,
+        "parity_sample": parity,
     }
     print(json.dumps(result), flush=True)
 
