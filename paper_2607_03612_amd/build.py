@@ -35,6 +35,23 @@ def command(out: str = LIB, extra=()) -> list:
     ]
 
 
+def device_asm(source: str, out: str) -> str:
+    """AMD assembly of one kernel source for gfx950 (device code only, the
+    same flags as the library), written to `out`."""
+    cmd = [
+        hipcc(), f"--offload-arch={ARCH}", "-O3", "-std=c++17",
+        "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+        "-Wno-unused-command-line-argument",
+        "-I", os.path.join(ROOT, "include"), "-I", CSRC,
+        "--cuda-device-only", "-S", os.path.join(CSRC, source), "-o", out,
+    ]
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    if res.returncode != 0:
+        sys.stderr.write(res.stdout + res.stderr)
+        raise RuntimeError(f"hipcc -S {source} failed with status {res.returncode}")
+    return out
+
+
 def build(verbose: bool = False) -> str:
     """Compile every source for gfx950 into the package's libsaf3r.so."""
     tmp = LIB + ".tmp"

@@ -15,10 +15,11 @@
 // and the P V product of half t-1 on the matrix cores while the VALU runs
 // the softmax of half t, and the scheduler is told to interleave the two
 // streams. Q sits in registers for the whole loop; K and V half tiles are
-// staged in LDS by the direct buffer-to-LDS load two steps ahead. All global
-// accesses use buffer instructions bounded by the head's extent, so a
-// partial last block reads zeros and a corrupt index list cannot touch
-// memory outside the head.
+// staged in LDS by the direct buffer-to-LDS load two steps ahead. Every
+// global access of Q, K, V and O is a buffer instruction whose range-checked
+// offsets (vector and immediate, never the unchecked scalar offset) are
+// bounded by the head's extent, so a partial last block reads zeros and a
+// corrupt index list cannot touch memory outside the head.
 //
 // Launch order: workgroup b runs on XCD b % 8; each XCD takes a contiguous
 // slab of query blocks of every head (neighbouring query blocks share kept
@@ -117,9 +118,9 @@ __device__ inline int swz(int r, int c) { return r * 128 + ((c ^ swz_f(r)) << 4)
 // Direct buffer-to-LDS loads of 8-row groups: instruction n fills LDS bytes
 // [1024n, 1024n + 1024), lane l its 16 bytes at 16l, i.e. row 8n + l/8,
 // slot l%8, which must hold chunk (l%8) ^ f(8n + l/8) = (l%8) ^ f(l/8) ^ (4
-// if n is odd). Rows past the head read as zeros. The lane's byte offset
-// inside its 8-row group depends only on the parity of n; the tile and
-// group offsets are wave-uniform and go in the scalar offset.
+// if n is odd). The lane's byte offset inside its 8-row group depends only
+// on the parity of n; the group offset 1024n is the instruction's immediate
+// offset, which the hardware adds to both the memory and the LDS address.
 struct DmaLaneOffsets {
   int even, odd;
 };
@@ -147,15 +148,23 @@ constexpr int kWaitVm0 = 0x0F70;   // vmcnt(0)
 constexpr int kWaitLgkm0 = 0xC07F; // lgkmcnt(0)
 
 // One 32-row half tile (rows 64j + 32h .. of the head) into an LDS half
-// buffer with the direct buffer-to-LDS load: four 1 KB instructions.
-__device__ inline void dma_half(__amdgpu_buffer_rsrc_t r, int j, int h, lds_char* buf,
-                                DmaLaneOffsets off) {
-  const int base = __builtin_amdgcn_readfirstlane((j * kBlock + 32 * h) * kHeadDim * 2);
-#pragma unroll
-  for (int n = 0; n < 4; ++n)
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)(buf + 1024 * n), 16,
-                                             (n & 1) ? off.odd : off.even,
-                                             base + n * 8 * kHeadDim * 2, 0, 0);
+// buffer with the direct buffer-to-LDS load: four 1 KB instructions. The
+// tile's offset goes into the base and extent of a descriptor built for this
+// tile in scalar registers, and the scalar offset operand stays 0: the
+// hardware range-checks the vector and immediate offsets against the extent
+// but not the scalar offset. So rows past the head's last token (a partial
+// last block) read zeros, and a block index outside [0, nb) reads a tile of
+// zeros instead of memory outside the head.
+__device__ inline void dma_half(const uint16_t* head, uint32_t head_bytes, int nb, int j, int h,
+                                lds_char* buf, DmaLaneOffsets off) {
+  const uint32_t t = __builtin_amdgcn_readfirstlane(
+      (uint32_t)j < (uint32_t)nb ? ((uint32_t)j * kBlock + 32u * h) * (kHeadDim * 2) : head_bytes);
+  const uint32_t rem = __builtin_amdgcn_readfirstlane(t < head_bytes ? head_bytes - t : 0u);
+  const __amdgpu_buffer_rsrc_t r = make_rsrc(reinterpret_cast<const char*>(head) + t, rem);
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)buf, 16, off.even, 0, 0, 0);
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)buf, 16, off.odd, 0, 1024, 0);
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)buf, 16, off.even, 0, 2048, 0);
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)buf, 16, off.odd, 0, 3072, 0);
 }
 
 // Key sets a launch walks: per-head lists or all blocks (kLists), every block
@@ -276,11 +285,13 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
   const __amdgpu_buffer_rsrc_t rk = make_rsrc(k + head_off, head_bytes);
   const __amdgpu_buffer_rsrc_t rv = make_rsrc(v + head_off, head_bytes);
   const __amdgpu_buffer_rsrc_t ro = make_rsrc(out + head_off, head_bytes);
-  auto load_half = [&](__amdgpu_buffer_rsrc_t r, int j, int h, lds_char* buf, DmaLaneOffsets off) {
+  const uint16_t* const kh = k + head_off;
+  const uint16_t* const vh = v + head_off;
+  auto load_half = [&](bool is_v, int j, int h, lds_char* buf, DmaLaneOffsets off) {
     if constexpr (kMode == kStrided)
-      dma_half_strided(r, j, h, buf, threadIdx.x, stride, a.n, head_bytes);
+      dma_half_strided(is_v ? rv : rk, j, h, buf, threadIdx.x, stride, a.n, head_bytes);
     else
-      dma_half(r, j, h, buf, off);
+      dma_half(is_v ? vh : kh, head_bytes, nb, j, h, buf, off);
   };
 
   // Q^T as the B operand: qB[tq][s] = Q[64i + 32tq + l32][16s + 8hf + (0..7)]
@@ -471,16 +482,16 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
   int j0 = tile_at(0), j1 = tile_at(1), j2 = tile_at(2);
   {
     // prologue: S^T of half 0, then the loads steps -2 and -1 would issue
-    load_half(rk, j0, 0, kbuf0, dma_off);
+    load_half(false, j0, 0, kbuf0, dma_off);
     __builtin_amdgcn_s_waitcnt(kWaitVm0);
     bf16x8 kA[4];
     read_k(kbuf0, kA);
     mfma_s(kA, s_cur);
     __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
-    load_half(rk, j0, 1, kbuf1, dma_off);   // K half 1 (tile 0)
-    load_half(rv, j0, 1, vbuf1, dma_off);   // V of half -1: any tile (its P is 0)
-    load_half(rk, j1, 0, kbuf0, dma_off);   // K half 2 (tile 1)
-    load_half(rv, j0, 0, vbuf0, dma_off);   // V half 0 (tile 0)
+    load_half(false, j0, 1, kbuf1, dma_off);   // K half 1 (tile 0)
+    load_half(true, j0, 1, vbuf1, dma_off);   // V of half -1: any tile (its P is 0)
+    load_half(false, j1, 0, kbuf0, dma_off);   // K half 2 (tile 1)
+    load_half(true, j0, 0, vbuf0, dma_off);   // V half 0 (tile 0)
   }
 
   // One step with the matrix-core and VALU work of the same step in one
@@ -523,8 +534,8 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
     // refill the two buffers this step read
     __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
     if constexpr (kNext) {
-      load_half(rk, jkn, h ^ 1, kb, dma_off);
-      load_half(rv, jvn, h ^ 1, vb, dma_off);
+      load_half(false, jkn, h ^ 1, kb, dma_off);
+      load_half(true, jvn, h ^ 1, vb, dma_off);
     }
 #pragma unroll
     for (int u = 0; u < 2; ++u)
