@@ -374,13 +374,6 @@ def baseline_stride(sigma: float) -> int:
 # whole layer
 
 
-def kept_fraction(lists_per_head, nb: int) -> float:
-    """Fraction of (query block, key block) pairs kept over all heads (heads
-    with block lists)."""
-    kept = sum(len(x) for lists in lists_per_head for x in lists)
-    return kept / (len(lists_per_head) * nb * nb)
-
-
 def run_layer(q, k, v, table, tokens_per_frame: int, dtype: str, block: int = 64,
               heads=None, with_attention: bool = True, features=None):
     """The whole hot path for one layer.
