@@ -85,8 +85,61 @@ def gpu_list(res, h, i):
     return res["idx"][h, i, :c]
 
 
-def check_lists(res, h, i, pattern, oracle_list, margin, nb, cap):
-    """Returns 'ok', 'near_tie' or raises AssertionError with the row named."""
+def ranking(pattern, param, score_row, tokens_per_frame=None):
+    """What a near-tie row's list is checked against: the oracle's score row
+    of a TOPK head (its probe scores for a GLOBAL_PROBE head) with the kept
+    count, or a COSINE_TOPK head's similarity row with the per-frame count.
+    None for the classes whose lists are fixed (no ranking)."""
+    if pattern in (2, 5):  # TOPK, GLOBAL_PROBE
+        return ("topk", np.asarray(score_row, np.float64), int(param))
+    if pattern == 6:  # COSINE_TOPK
+        return ("cosine", np.asarray(score_row, np.float64), int(param), int(tokens_per_frame))
+    return None
+
+
+def valid_topk(got, scores, k, tol=NEAR_TIE):
+    """True when the ascending, distinct blocks `got` are a top-k of `scores`
+    up to `tol`: exactly k blocks, every kept score at least s_(k) - tol and
+    every dropped score at most s_(k+1) + tol, with s_(r) the r-th largest
+    oracle score."""
+    got = np.asarray(got, np.int64)
+    nb = len(scores)
+    if len(got) != k or k < 1 or k > nb:
+        return False
+    ranked = np.sort(scores)[::-1]
+    kept = np.zeros(nb, bool)
+    kept[got] = True
+    if scores[kept].min() < ranked[k - 1] - tol:
+        return False
+    return k == nb or scores[~kept].max() <= ranked[k] + tol
+
+
+def valid_ranking(got, rank, block=64):
+    """`valid_topk` for a TOPK / GLOBAL_PROBE row, or per frame for a
+    COSINE_TOPK row (the frame's min(k, blocks) most similar blocks, a block
+    counted under the frame of its first token)."""
+    import oracle as O
+
+    if rank[0] == "topk":
+        return valid_topk(got, rank[1], rank[2])
+    _, sim, k, T = rank
+    frame = np.array([O.block_frame(j, T, block) for j in range(len(sim))])
+    got = np.asarray(got, np.int64)
+    for f in np.unique(frame):
+        js = np.nonzero(frame == f)[0]
+        mine = np.searchsorted(js, got[frame[got] == f])
+        if not valid_topk(mine, sim[js], min(k, len(js))):
+            return False
+    return True
+
+
+def check_lists(res, h, i, pattern, oracle_list, margin, nb, cap, rank=None):
+    """Returns 'ok', 'near_tie' or raises AssertionError with the row named.
+
+    Lists must equal the oracle's where its margin exceeds NEAR_TIE. A
+    near-tie row must still be a valid top-k of the oracle's ranking `rank`
+    (see `ranking`); its outputs are then compared with the oracle run on
+    the GPU's own list."""
     c = int(res["cnt"][h, i])
     if pattern == 0:  # DENSE: count only, list not materialised
         assert c == nb, f"head {h} block {i}: dense count {c} != {nb}"
@@ -97,7 +150,9 @@ def check_lists(res, h, i, pattern, oracle_list, margin, nb, cap):
     assert np.all(np.diff(got) > 0), f"head {h} block {i}: list not strictly ascending"
     assert got.min() >= 0 and got.max() < nb
     if margin <= NEAR_TIE:
-        assert c == len(oracle_list)
+        assert rank is not None, f"head {h} block {i}: near-tie row checked without the oracle's ranking"
+        assert c == len(oracle_list) and valid_ranking(got, rank), \
+            f"head {h} block {i}: near-tie list {list(got)} is not a valid top-k (oracle {list(oracle_list)})"
         return "near_tie"
     assert c == len(oracle_list) and np.array_equal(got, oracle_list), \
         f"head {h} block {i}: gpu {list(got)} != oracle {list(oracle_list)} (margin {margin})"
@@ -121,4 +176,5 @@ def finite(x):
 
 
 __all__ = ["NEAR_TIE", "TOL_BF16", "TOL_F32", "gpu_layer", "attention_workspace", "check_lists", "max_abs",
-           "sample_blocks", "to_device", "out_to_numpy", "gpu_list", "math"]
+           "sample_blocks", "to_device", "out_to_numpy", "gpu_list", "ranking", "valid_topk",
+           "valid_ranking", "math"]
