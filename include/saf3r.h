@@ -19,7 +19,12 @@
  *   - Blocks are 64 tokens: block b holds tokens [64b, min(64b+64, N)); the
  *     last block may be partial. nb = ceil(N / 64).
  *   - Every device pointer is owned by the caller, must be valid for the
- *     sizes stated, and must not alias another argument. The library
+ *     sizes stated, and must not alias another argument.
+ *   - Alignment: Q, K, V, O, q_pooled, the NMSE inputs and every workspace
+ *     are read or written with 16-byte vector accesses and must be 16-byte
+ *     aligned; k_pooled, scores and nmse_out 8-byte; block_idx, block_cnt
+ *     and lse 4-byte; cosine features to their element size. A misaligned
+ *     pointer returns SAF3R_ERR_INVALID_ARGUMENT. The library
  *     allocates nothing and keeps no state between calls; calls on different
  *     streams may run concurrently when their outputs do not overlap.
  *   - `problem` and `table` are host pointers read during the call only.
@@ -40,7 +45,7 @@ extern "C" {
 
 typedef enum {
   SAF3R_OK = 0,
-  SAF3R_ERR_INVALID_ARGUMENT = -1, /* null pointer, non-positive size, bad dtype */
+  SAF3R_ERR_INVALID_ARGUMENT = -1, /* null or misaligned pointer, non-positive size, bad dtype */
   SAF3R_ERR_UNSUPPORTED = -2,      /* head_dim or block other than 64, sizes beyond the limits */
   SAF3R_ERR_CAPACITY = -3,         /* cap or a workspace smaller than required */
   SAF3R_ERR_HIP = -4,              /* the HIP runtime reported an error on launch */
@@ -192,13 +197,20 @@ int64_t saf3r_select_workspace_bytes(const saf3r_problem* problem, const saf3r_h
  *   lse[t] = log(sum_u exp(z_u))            (natural log)
  * bf16 inputs: Q K^T and P V on bf16 matrix cores with fp32 accumulation, the
  * softmax in fp32, P rounded to bf16 for P V and for the row sum that
- * normalises out and gives lse, out rounded to bf16. fp32
- * inputs: everything in fp32.
+ * normalises out and gives lse, out rounded to bf16. So on this path lse is
+ * the log of the sum of the bf16-rounded weights exp(z_u - max) plus max: it
+ * differs from the fp32 log-sum-exp by up to 2^-8 (bf16's relative rounding
+ * of each weight), and a caller that merges lse across launches inherits that
+ * bias. fp32 inputs: everything in fp32.
  *   q, k, v      device [heads, N, 64] of problem->dtype
  *   block_idx, block_cnt, cap   as written by saf3r_select_blocks; entries of
  *                DENSE and STRIDE heads are not read. A list that is not
  *                ascending, repeats a block or holds indices outside [0, nb)
- *                gives unspecified output values but no out-of-bounds access.
+ *                gives unspecified output values but no access outside the
+ *                head's N rows of Q, K, V and O: every K/V tile is read
+ *                through a buffer descriptor bounded by the head's extent
+ *                (an index outside [0, nb) reads a tile of zeros, and so do
+ *                the rows past N of a partial last block).
  *   out          device [heads, N, 64] of problem->dtype
  *   lse_or_null  NULL, or device float32 [heads, N]
  *   workspace_or_null, workspace_bytes

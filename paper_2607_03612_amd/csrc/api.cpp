@@ -127,6 +127,11 @@ int capacity(const Shape& s, const saf3r_head_cfg* t) {
 
 bool pooled_class(int pattern) { return pattern == SAF3R_TOPK || pattern == SAF3R_GLOBAL_PROBE; }
 
+// True when p is null or a multiple of `bytes`: the kernels read and write
+// Q/K/V/O, the pooled arrays, the NMSE inputs and the workspaces with
+// 16-byte vector accesses, the other arrays element by element.
+bool aligned(const void* p, uintptr_t bytes) { return reinterpret_cast<uintptr_t>(p) % bytes == 0; }
+
 saf3r_status hip_status(hipError_t e) { return e == hipSuccess ? SAF3R_OK : SAF3R_ERR_HIP; }
 
 }  // namespace
@@ -157,6 +162,8 @@ saf3r_status saf3r_estimate_blocks(const saf3r_problem* problem, const saf3r_hea
   st = check_table(s, table);
   if (st != SAF3R_OK) return st;
   if (!q || !k || !q_pooled || !k_pooled) return SAF3R_ERR_INVALID_ARGUMENT;
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(q_pooled, 16) || !aligned(k_pooled, 8))
+    return SAF3R_ERR_INVALID_ARGUMENT;
   saf3r::PoolArgs a{};
   a.n = s.n;
   a.nb = s.nb;
@@ -188,6 +195,9 @@ saf3r_status saf3r_select_blocks(const saf3r_problem* problem, const saf3r_head_
   st = check_table(s, table);
   if (st != SAF3R_OK) return st;
   if (!q_pooled || !k_pooled || !block_idx || !block_cnt) return SAF3R_ERR_INVALID_ARGUMENT;
+  if (!aligned(q_pooled, 8) || !aligned(k_pooled, 8) || !aligned(block_idx, 4) ||
+      !aligned(block_cnt, 4) || !aligned(scores_or_null, 8) || !aligned(workspace_or_null, 16))
+    return SAF3R_ERR_INVALID_ARGUMENT;
   if (cap < capacity(s, table)) return SAF3R_ERR_CAPACITY;
 
   saf3r::TopKArgs ta{};
@@ -310,6 +320,9 @@ saf3r_status saf3r_sparse_attention(const saf3r_problem* problem, const saf3r_he
   st = check_table(s, table);
   if (st != SAF3R_OK) return st;
   if (!q || !k || !v || !out) return SAF3R_ERR_INVALID_ARGUMENT;
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 16) ||
+      !aligned(block_idx, 4) || !aligned(block_cnt, 4) || !aligned(lse_or_null, 4))
+    return SAF3R_ERR_INVALID_ARGUMENT;
   bool needs_lists = false;
   for (int h = 0; h < s.heads; ++h) {
     const int p = table[h].pattern;
@@ -323,8 +336,7 @@ saf3r_status saf3r_sparse_attention(const saf3r_problem* problem, const saf3r_he
   if (split_bytes < 0) return (saf3r_status)split_bytes;
   const bool split = workspace_or_null != nullptr && split_bytes > 0;
   if (workspace_or_null) {
-    if (workspace_bytes < 0 || reinterpret_cast<uintptr_t>(workspace_or_null) % 16 != 0)
-      return SAF3R_ERR_INVALID_ARGUMENT;
+    if (workspace_bytes < 0 || !aligned(workspace_or_null, 16)) return SAF3R_ERR_INVALID_ARGUMENT;
     if (workspace_bytes < split_bytes) return SAF3R_ERR_CAPACITY;
   }
 
@@ -422,6 +434,9 @@ saf3r_status saf3r_cosine_select(const saf3r_problem* problem, const saf3r_head_
   if (st != SAF3R_OK) return st;
   if (!features || !workspace || !block_idx || !block_cnt) return SAF3R_ERR_INVALID_ARGUMENT;
   if (feat_dim < 1 || feat_dim > saf3r::kMaxCosineDim) return SAF3R_ERR_INVALID_ARGUMENT;
+  if (!aligned(features, s.dtype == SAF3R_BF16 ? 2 : 4) || !aligned(workspace, 8) ||
+      !aligned(block_idx, 4) || !aligned(block_cnt, 4))
+    return SAF3R_ERR_INVALID_ARGUMENT;
   const int64_t need = saf3r_cosine_workspace_bytes(problem, feat_dim);
   if (workspace_bytes < need) return SAF3R_ERR_CAPACITY;
   if (cap < capacity(s, table)) return SAF3R_ERR_CAPACITY;
@@ -466,6 +481,9 @@ saf3r_status saf3r_nmse(const saf3r_problem* problem, const void* o_full, const 
   const saf3r_status st = check_problem(problem, &s);
   if (st != SAF3R_OK) return st;
   if (!o_full || !o_sparse || !workspace || !nmse_out) return SAF3R_ERR_INVALID_ARGUMENT;
+  if (!aligned(o_full, 16) || !aligned(o_sparse, 16) || !aligned(workspace, 16) ||
+      !aligned(nmse_out, 8))
+    return SAF3R_ERR_INVALID_ARGUMENT;
   if (workspace_bytes < saf3r_nmse_workspace_bytes(problem)) return SAF3R_ERR_CAPACITY;
   return hip_status(saf3r::launch_nmse(s.dtype, o_full, o_sparse, workspace, nmse_out, s.heads,
                                        s.n, static_cast<hipStream_t>(stream)));
@@ -474,7 +492,7 @@ saf3r_status saf3r_nmse(const saf3r_problem* problem, const void* o_full, const 
 const char* saf3r_status_string(int32_t status) {
   switch (status) {
     case SAF3R_OK: return "ok";
-    case SAF3R_ERR_INVALID_ARGUMENT: return "invalid argument (null pointer, size or dtype)";
+    case SAF3R_ERR_INVALID_ARGUMENT: return "invalid argument (null or misaligned pointer, size or dtype)";
     case SAF3R_ERR_UNSUPPORTED: return "unsupported (head_dim/block must be 64; size limits)";
     case SAF3R_ERR_CAPACITY: return "index capacity or workspace smaller than required";
     case SAF3R_ERR_HIP: return "HIP runtime error on launch";

@@ -240,3 +240,46 @@ def test_missing_library_fails_loudly(B, tmp_path, monkeypatch):
         B.index_capacity([(B.TOPK, 4)], 2, 100)
     with pytest.raises(RuntimeError, match="missing"):
         B.attention_workspace_bytes([(B.TOPK, 4)], 2, 100)
+
+
+def test_misaligned_pointers_are_rejected(B):
+    """Every pointer the header requires to be aligned is checked before any
+    launch: 16 bytes for Q/K/V/O, q_pooled, the NMSE inputs and workspaces;
+    8 for k_pooled, scores and nmse_out; 4 for lists, counts and lse."""
+    lib = B.load()
+    p = _p(B, heads=2, frames=2, T=100)  # nb = 4
+    t = B.head_table([(B.FRAME_LOCAL, 0), (B.TOPK, 2)])
+    ok = ctypes.c_void_p(0x1000)
+    a8, a4, a2 = ctypes.c_void_p(0x1008), ctypes.c_void_p(0x1004), ctypes.c_void_p(0x1002)
+    est = lib.saf3r_estimate_blocks
+    for args in ((a8, ok, ok, ok), (ok, a8, ok, ok), (ok, ok, a8, ok), (ok, ok, ok, a4)):
+        assert est(ctypes.byref(p), t, *args, None) == -1, args
+    sel = lib.saf3r_select_blocks
+    need = lib.saf3r_select_workspace_bytes(ctypes.byref(p), t)
+    for args in ((a4, ok, ok, ok, None, None), (ok, a4, ok, ok, None, None),
+                 (ok, ok, a2, ok, None, None), (ok, ok, ok, a2, None, None),
+                 (ok, ok, ok, ok, a4, None), (ok, ok, ok, ok, None, a8)):
+        qp, kp, idx, cnt, scores, ws = args
+        assert sel(ctypes.byref(p), t, qp, kp, idx, cnt, 8, scores, ws, need, None) == -1, args
+    att = lib.saf3r_sparse_attention
+    for args in ((a8, ok, ok, ok, ok, ok, None), (ok, a8, ok, ok, ok, ok, None),
+                 (ok, ok, a8, ok, ok, ok, None), (ok, ok, ok, ok, ok, a8, None),
+                 (ok, ok, ok, a2, ok, ok, None), (ok, ok, ok, ok, a2, ok, None),
+                 (ok, ok, ok, ok, ok, ok, a2)):
+        q, k, v, idx, cnt, out, lse = args
+        assert att(ctypes.byref(p), t, q, k, v, idx, cnt, 8, out, lse, None, 0, None) == -1, args
+    assert att(ctypes.byref(p), t, ok, ok, ok, ok, ok, 8, ok, None, a8, 1 << 20, None) == -1
+    ct = B.head_table([(B.COSINE_TOPK, 1), (B.DENSE, 0)])
+    cneed = lib.saf3r_cosine_workspace_bytes(ctypes.byref(p), 64)
+    cos = lib.saf3r_cosine_select
+    for args in ((ctypes.c_void_p(0x1001), ok, ok, ok), (ok, a4, ok, ok), (ok, ok, a2, ok),
+                 (ok, ok, ok, a2)):
+        f, ws, idx, cnt = args
+        assert cos(ctypes.byref(p), ct, f, 64, ws, cneed, idx, cnt, 8, None) == -1, args
+    pf = _p(B, heads=2, frames=2, T=100, dtype=B.F32)
+    assert cos(ctypes.byref(pf), ct, a2, 64, ok, cneed, ok, ok, 8, None) == -1  # fp32: 4 bytes
+    nm = lib.saf3r_nmse
+    nneed = lib.saf3r_nmse_workspace_bytes(ctypes.byref(p))
+    for args in ((a8, ok, ok, ok), (ok, a8, ok, ok), (ok, ok, a8, ok), (ok, ok, ok, a4)):
+        f, s, ws, o = args
+        assert nm(ctypes.byref(p), f, s, ws, nneed, o, None) == -1, args
