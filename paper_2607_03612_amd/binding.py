@@ -3,6 +3,8 @@
 Every computation runs in the HIP library; PyTorch only provides device
 memory and the current HIP stream. Names mirror the C ABI without the
 ``saf3r_`` prefix. If the library has not been built, ``load()`` raises.
+The library is ``libsaf3r.so`` next to this file, or the file the
+environment variable ``SAF3R_LIBRARY`` names.
 """
 from __future__ import annotations
 
@@ -10,7 +12,7 @@ import ctypes
 import os
 
 PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(PKG, "libsaf3r.so")
+LIB_PATH = os.environ.get("SAF3R_LIBRARY") or os.path.join(PKG, "libsaf3r.so")
 
 F32, BF16 = 0, 1
 DENSE, FRAME_LOCAL, TOPK, ANCHOR, STRIDE, GLOBAL_PROBE, COSINE_TOPK, SKIP = 0, 1, 2, 3, 4, 5, 6, 7
@@ -80,9 +82,10 @@ def _declare(lib):
     lib.saf3r_status_string.restype = ctypes.c_char_p
 
 
-def load(path: str = LIB_PATH):
+def load(path: str = None):
     """Load the HIP library (raises if it has not been built)."""
     global _LIB
+    path = path or LIB_PATH
     if _LIB is None:
         if not os.path.exists(path):
             raise RuntimeError(

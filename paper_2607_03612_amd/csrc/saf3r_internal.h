@@ -134,14 +134,23 @@ hipError_t launch_attention(int dtype, const void* q, const void* k, const void*
 hipError_t launch_attention_merge(const float* part_o, const float* part_ml, void* out,
                                   float* lse, const MergeArgs& a, hipStream_t s);
 
-// Bytes of LDS the Top-K selection kernel needs for `rows` query blocks.
-size_t topk_lds_bytes(int rows, int nb);
-// workspace path of the Top-K selection: bytes of one query block's key row,
-// and the two launches (scores into `keys`, then one wave per row)
-size_t topk_ws_row_bytes(int nb);
+// Top-K selection sizes, shared by the kernels and the host layer. Key
+// slots per lane for a row of nb blocks: ceil(nb / 64) rounded up to a
+// multiple of 4; a row occupies 64 * row_chunk(nb) words (LDS or workspace).
+__host__ __device__ constexpr int row_chunk(int nb) { return ((nb + 63) / 64 + 3) & ~3; }
+// LDS entries after the last row, so that every lane may read its C slots
+// rounded up to a multiple of 8 unconditionally.
+constexpr int kRowPad = 128;
+// Bytes of LDS the single-launch Top-K selection needs for `rows` query blocks.
+inline size_t topk_lds_bytes(int rows, int nb) {
+  return ((size_t)rows * 64 * row_chunk(nb) + kRowPad) * sizeof(uint32_t);
+}
+// Threads per workgroup of the single-launch Top-K selection for `rows` query blocks.
+inline int topk_threads(int rows) { return rows >= 16 ? 512 : 256; }
+// Workspace path of the Top-K selection: bytes of one query block's key row.
+inline size_t topk_ws_row_bytes(int nb) { return (size_t)64 * row_chunk(nb) * sizeof(uint32_t); }
+// The workspace path's two launches (scores into `keys`, then one wave per row).
 hipError_t launch_select_topk_ws(const double* qp, const double* kpT, uint32_t* keys, int32_t* idx,
                                  int32_t* cnt, double* scores, const TopKArgs& a, hipStream_t s);
-// Threads per workgroup of the Top-K selection kernel for `rows` query blocks.
-int topk_threads(int rows);
 
 }  // namespace saf3r

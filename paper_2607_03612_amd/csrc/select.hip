@@ -127,9 +127,6 @@ __device__ inline f64x4 score_tile(const QOperand& q, const KColumn& k) {
 // hold 0, below every valid key.
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-// Key slots per lane for a row of nb blocks: ceil(nb / 64) rounded up to a
-// multiple of 4; a row occupies 64 * row_chunk(nb) words of LDS.
-__host__ __device__ inline int row_chunk(int nb) { return ((nb + 63) / 64 + 3) & ~3; }
 
 template <int MAXK>
 struct RowKeys {
@@ -217,9 +214,6 @@ __device__ inline uint32_t kth_largest(uint32_t lo, uint32_t hi_incl, int k, Cou
   return (uint32_t)lo64;
 }
 
-// LDS entries after the last row, so that every lane may read its C slots
-// rounded up to a multiple of 8 unconditionally.
-constexpr int kRowPad = 128;
 
 // Candidates packed per wave once the bracket holds at most this many keys
 // (8 per lane), and the pivots' distance from the target sample rank.
@@ -823,11 +817,6 @@ hipError_t launch_topk_rows(const double* qp, const double* kpT, int32_t* idx, i
 
 }  // namespace
 
-size_t topk_lds_bytes(int rows, int nb) {
-  return ((size_t)rows * 64 * row_chunk(nb) + kRowPad) * sizeof(uint32_t);
-}
-
-int topk_threads(int rows) { return rows >= 16 ? 512 : 256; }
 
 hipError_t launch_select_topk(const double* qp, const double* kpT, int32_t* idx, int32_t* cnt,
                               double* scores, const TopKArgs& a, size_t lds, hipStream_t s) {
@@ -842,7 +831,6 @@ hipError_t launch_select_topk(const double* qp, const double* kpT, int32_t* idx,
   }
 }
 
-size_t topk_ws_row_bytes(int nb) { return (size_t)64 * row_chunk(nb) * sizeof(uint32_t); }
 
 hipError_t launch_select_topk_ws(const double* qp, const double* kpT, uint32_t* keys, int32_t* idx,
                                  int32_t* cnt, double* scores, const TopKArgs& a, hipStream_t s) {
