@@ -290,6 +290,23 @@ saf3r_status saf3r_nmse(const saf3r_problem* problem, const void* o_full, const 
                         void* workspace, int64_t workspace_bytes, double* nmse_out,
                         void* stream);
 
+/* saf3r_nmse without a workspace, for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid allocation). The per-slice partial sums go to a 512 KB array that
+ * the library holds on each GPU it runs on, until the process ends; it fits
+ * every head count the library accepts (up to 256), and a problem that
+ * would need more returns SAF3R_ERR_CAPACITY. Results are the same bits as
+ * saf3r_nmse's. The first call on a device resolves the array's address
+ * (hipGetSymbolAddress), so make it outside graph capture. Calls on one GPU
+ * share the array: calls that overlap (on streams with no ordering between
+ * them) race and give undefined results.
+ *   o_full, o_sparse, nmse_out   as for saf3r_nmse
+ * Returns SAF3R_OK; SAF3R_ERR_INVALID_ARGUMENT for a null or misaligned
+ * pointer; SAF3R_ERR_HIP if the array's address cannot be resolved; nothing
+ * is enqueued on an error. */
+saf3r_status saf3r_nmse_noalloc(const saf3r_problem* problem, const void* o_full,
+                                const void* o_sparse, double* nmse_out, void* stream);
+
 /* Static description of a status code (never NULL). */
 const char* saf3r_status_string(int32_t status);
 

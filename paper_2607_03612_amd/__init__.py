@@ -21,6 +21,7 @@ from .binding import (  # noqa: F401
     index_capacity,
     load,
     nmse,
+    nmse_noalloc,
     nmse_workspace_bytes,
     num_blocks,
     run_layer,

@@ -31,6 +31,7 @@ EXPORTS = (
     "saf3r_cosine_select",
     "saf3r_nmse_workspace_bytes",
     "saf3r_nmse",
+    "saf3r_nmse_noalloc",
     "saf3r_status_string",
 )
 
@@ -78,6 +79,8 @@ def _declare(lib):
     lib.saf3r_nmse_workspace_bytes.restype = ctypes.c_int64
     lib.saf3r_nmse.argtypes = [P, V, V, V, ctypes.c_int64, V, V]
     lib.saf3r_nmse.restype = I32
+    lib.saf3r_nmse_noalloc.argtypes = [P, V, V, V, V]
+    lib.saf3r_nmse_noalloc.restype = I32
     lib.saf3r_status_string.argtypes = [I32]
     lib.saf3r_status_string.restype = ctypes.c_char_p
 
@@ -320,6 +323,18 @@ def nmse(o_full, o_sparse, frames, tokens_per_frame, out=None, workspace=None, s
     _check(_lib().saf3r_nmse(ctypes.byref(p), _ptr(o_full), _ptr(o_sparse), _ptr(workspace),
                              ctypes.c_int64(workspace.numel() * workspace.element_size()),
                              _ptr(out), _stream(stream)), "saf3r_nmse")
+    return out
+
+
+def nmse_noalloc(o_full, o_sparse, frames, tokens_per_frame, out, stream=None):
+    """``nmse`` through the entry point that allocates nothing: the library's
+    own per-GPU array holds the partial sums. ``out``: float64 ``[H]`` device
+    tensor the caller provides."""
+    _check_qkv(o_full, o_sparse)
+    H, N, _ = o_full.shape
+    p = problem(H, frames, tokens_per_frame, _torch_dtype_code(o_full))
+    _check(_lib().saf3r_nmse_noalloc(ctypes.byref(p), _ptr(o_full), _ptr(o_sparse), _ptr(out),
+                                     _stream(stream)), "saf3r_nmse_noalloc")
     return out
 
 

@@ -489,6 +489,21 @@ saf3r_status saf3r_nmse(const saf3r_problem* problem, const void* o_full, const 
                                        s.n, static_cast<hipStream_t>(stream)));
 }
 
+saf3r_status saf3r_nmse_noalloc(const saf3r_problem* problem, const void* o_full,
+                                const void* o_sparse, double* nmse_out, void* stream) {
+  Shape s;
+  const saf3r_status st = check_problem(problem, &s);
+  if (st != SAF3R_OK) return st;
+  if (!o_full || !o_sparse || !nmse_out) return SAF3R_ERR_INVALID_ARGUMENT;
+  if (!aligned(o_full, 16) || !aligned(o_sparse, 16) || !aligned(nmse_out, 8))
+    return SAF3R_ERR_INVALID_ARGUMENT;
+  if (saf3r_nmse_workspace_bytes(problem) > saf3r::kNmseScratchBytes) return SAF3R_ERR_CAPACITY;
+  void* scratch = nullptr;
+  if (saf3r::nmse_scratch(&scratch) != hipSuccess) return SAF3R_ERR_HIP;
+  return hip_status(saf3r::launch_nmse(s.dtype, o_full, o_sparse, scratch, nmse_out, s.heads, s.n,
+                                       static_cast<hipStream_t>(stream)));
+}
+
 const char* saf3r_status_string(int32_t status) {
   switch (status) {
     case SAF3R_OK: return "ok";

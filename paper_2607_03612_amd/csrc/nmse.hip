@@ -7,9 +7,20 @@
 //      head's outputs (16-byte loads, four in flight per thread) and write
 //      their (numerator, denominator) pair to the workspace;
 //   2. one wave per head adds its kNmseParts pairs and divides.
+#include <atomic>
+
 #include "saf3r_internal.h"
 
 namespace saf3r {
+
+// Partial sums of saf3r_nmse_noalloc: the (numerator, denominator) pairs of
+// up to kMaxHeads heads, kNmseScratchBytes (512 KB), which each GPU the
+// library runs on holds until the process ends. Host code never passes this
+// name to a kernel (on the host it is a stand-in, not a device address): the
+// array's device address comes from hipGetSymbolAddress, once per device.
+static __device__ __align__(256) double2 scratch[kMaxHeads * kNmseParts];
+static_assert(sizeof(scratch) == kNmseScratchBytes, "scratch size");
+
 namespace {
 
 constexpr int kNmseThreads = 256;
@@ -110,6 +121,25 @@ __global__ __launch_bounds__(64) void nmse_final_kernel(const double2* __restric
 }
 
 }  // namespace
+
+hipError_t nmse_scratch(void** ptr) {
+  // one resolved address per device, kept for the life of the process
+  constexpr int kMaxDevices = 64;
+  static std::atomic<void*> resolved[kMaxDevices];
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  void* p = resolved[dev].load(std::memory_order_acquire);
+  if (p == nullptr) {
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (p == nullptr) return hipErrorInvalidSymbol;
+    resolved[dev].store(p, std::memory_order_release);
+  }
+  *ptr = p;
+  return hipSuccess;
+}
 
 hipError_t launch_nmse(int dtype, const void* ref, const void* test, void* workspace, double* out,
                        int heads, int64_t n, hipStream_t s) {

@@ -24,6 +24,9 @@ enum Pattern : int32_t {
 constexpr int kMaxCosineDim = 4096;   // feature width accepted by the cosine selection
 constexpr int kMaxCosinePerFrame = 64;  // key blocks kept per frame by a cosine head
 constexpr int kNmseParts = 128;         // NMSE partial sums per head (workspace pairs)
+// Device array of saf3r_nmse_noalloc's partial sums: every head count the
+// library accepts (one float64 pair per part).
+constexpr int64_t kNmseScratchBytes = (int64_t)kMaxHeads * kNmseParts * 16;
 
 // ---------------------------------------------------------------- launches
 
@@ -128,6 +131,9 @@ hipError_t launch_cosine(int dtype, const void* f, double* fb, double* sim, int3
                          int32_t* cnt, const CosineArgs& a, hipStream_t s);
 hipError_t launch_nmse(int dtype, const void* ref, const void* test, void* workspace, double* out,
                        int heads, int64_t n, hipStream_t s);
+// Device address of the current device's NMSE scratch array (resolved on the
+// first call on that device).
+hipError_t nmse_scratch(void** ptr);
 hipError_t launch_attention(int dtype, const void* q, const void* k, const void* v,
                             const int32_t* idx, const int32_t* cnt, void* out, float* lse,
                             const AttnArgs& a, hipStream_t s);

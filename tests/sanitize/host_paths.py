@@ -59,6 +59,7 @@ def test_valid_calls_reach_consistent_launches(heads, frames, T, table, dtype):
         assert lib.saf3r_cosine_select(ctypes.byref(p), t, OK, 96, OK, cws, OK, OK, cap, None) == 0
     nws = lib.saf3r_nmse_workspace_bytes(ctypes.byref(p))
     assert lib.saf3r_nmse(ctypes.byref(p), OK, OK, OK, nws, OK, None) == 0
+    assert lib.saf3r_nmse_noalloc(ctypes.byref(p), OK, OK, OK, None) == 0
 
 
 def test_all_dense_table_is_one_launch():

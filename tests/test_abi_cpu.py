@@ -283,3 +283,21 @@ def test_misaligned_pointers_are_rejected(B):
     for args in ((a8, ok, ok, ok), (ok, a8, ok, ok), (ok, ok, a8, ok), (ok, ok, ok, a4)):
         f, s, ws, o = args
         assert nm(ctypes.byref(p), f, s, ws, nneed, o, None) == -1, args
+
+
+def test_nmse_noalloc_validates_before_launch(B):
+    """The allocation-free NMSE entry point checks its arguments like
+    saf3r_nmse before it touches the device."""
+    lib = B.load()
+    p = _p(B, heads=3, frames=8, T=1374)
+    ok, a8, a4 = ctypes.c_void_p(0x1000), ctypes.c_void_p(0x1008), ctypes.c_void_p(0x1004)
+    nm = lib.saf3r_nmse_noalloc
+    assert nm(None, ok, ok, ok, None) == -1
+    assert nm(ctypes.byref(_p(B, heads=0)), ok, ok, ok, None) == -1
+    assert nm(ctypes.byref(_p(B, heads=257)), ok, ok, ok, None) == -2
+    assert nm(ctypes.byref(p), None, ok, ok, None) == -1
+    assert nm(ctypes.byref(p), ok, None, ok, None) == -1
+    assert nm(ctypes.byref(p), ok, ok, None, None) == -1
+    assert nm(ctypes.byref(p), a8, ok, ok, None) == -1
+    assert nm(ctypes.byref(p), ok, a8, ok, None) == -1
+    assert nm(ctypes.byref(p), ok, ok, a4, None) == -1
