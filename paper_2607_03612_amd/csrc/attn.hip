@@ -521,14 +521,14 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
     probs(s_cur, p_new, rs);
     // schedule of this region: the 12 LDS operand reads first (mask 0x100),
     // ten softmax VALU ops (0x002) while they land, then each of the 16
-    // MFMAs (0x008) followed by five VALU ops, so the matrix cores and the
+    // MFMAs (0x008) followed by four VALU ops, so the matrix cores and the
     // VALU work on independent data side by side
     __builtin_amdgcn_sched_group_barrier(0x100, 12, 0);
     __builtin_amdgcn_sched_group_barrier(0x002, 10, 0);
 #pragma unroll
     for (int g = 0; g < 16; ++g) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
     }
     fixup(s_cur, p_new, rs);
     // refill the two buffers this step read
