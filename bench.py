@@ -16,6 +16,7 @@ from __future__ import annotations
 import argparse
 import hashlib
 import json
+import math
 import os
 import sys
 import time
@@ -435,6 +436,117 @@ def run_stack(args, P, torch, w):
     print(json.dumps(result), flush=True)
 
 
+def other_config(P, torch, name, steps, warmup, seed=0):
+    """One smaller configuration timed the way the main workload is (estimate
+    -> select -> attention on one resident layer, HIP events on the launch
+    stream), with the attention kernel against its dtype's matrix peak and,
+    on every query block of a layer of at most 20000 tokens (else a seeded
+    sample of 16 per head), its lists and outputs against the oracle."""
+    import oracle as O
+    from workloads import WORKLOADS, make_qkv, make_table
+
+    w = WORKLOADS[name]
+    q, k, v = make_qkv(w, seed=seed)
+    table = make_table(w, seed=seed)
+    code = P.BF16 if w.dtype == "bf16" else P.F32
+
+    def up(x):
+        if w.dtype == "bf16":
+            return torch.from_numpy(x.view(np.int16)).cuda().view(torch.bfloat16)
+        return torch.from_numpy(x).cuda()
+
+    tq, tk, tv = up(q), up(k), up(v)
+    H, N, nb, S, T = w.heads, w.tokens, w.nb, w.frames, w.tokens_per_frame
+    dev = tq.device
+    cap = P.index_capacity(table, S, T, code)
+    qp = torch.zeros((H, nb, 64), dtype=torch.float64, device=dev)
+    kp = torch.zeros((H, 64, nb), dtype=torch.float64, device=dev)
+    idx = torch.empty((H, nb, cap), dtype=torch.int32, device=dev)
+    cnt = torch.empty((H, nb), dtype=torch.int32, device=dev)
+    out = torch.empty_like(tq)
+    sel_ws = torch.empty(max(P.select_workspace_bytes(table, S, T, code), 16) // 4, dtype=torch.int32,
+                         device=dev)
+    att_ws = torch.empty(max(P.attention_workspace_bytes(table, S, T, code), 16) // 4,
+                         dtype=torch.int32, device=dev)
+
+    def step(ev=None):
+        if ev:
+            ev[0].record()
+        P.estimate_blocks(tq, tk, table, S, T, qp, kp)
+        if ev:
+            ev[1].record()
+        P.select_blocks(qp, kp, table, S, T, cap, idx, cnt, dtype=code, workspace=sel_ws)
+        if ev:
+            ev[2].record()
+        P.sparse_attention(tq, tk, tv, table, S, T, idx, cnt, out, workspace=att_ws)
+        if ev:
+            ev[3].record()
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
+    a0, a1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a0.record()
+    for st in range(steps):
+        step(evs[st])
+    a1.record()
+    torch.cuda.synchronize()
+    ms_step = a0.elapsed_time(a1) / steps
+    ph = [float(np.mean([e[i].elapsed_time(e[i + 1]) for e in evs])) for i in range(3)]
+    idx_h, cnt_h = idx.cpu().numpy(), cnt.cpu().numpy()
+    flops = kept_flops(idx_h, cnt_h, table, N, nb)
+    peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
+    att_tflops = flops / (ph[2] * 1e-3) / 1e12
+    kept_pairs = sum(nb * nb if p == 0 else int(cnt_h[h].sum()) for h, (p, _) in enumerate(table))
+    # parity: every query block of a small layer, a sample of a larger one
+    rows = list(range(nb)) if N <= 20000 else sample_rows(nb, 16, seed)
+    got = out.float().cpu().numpy().astype(np.float64)
+    tol = 2e-2 if w.dtype == "bf16" else 1e-4
+    equal = near = mismatch = 0
+    err = 0.0
+    from tests.parity import valid_topk
+
+    for h, (pattern, param) in enumerate(table):
+        qh, kh, vh = (O.to_f64(x[h], w.dtype) for x in (q, k, v))
+        kbar = O.pool_blocks(kh, 64) if pattern == O.TOPK else None
+        for i in rows:
+            r = O.block_range(i, N, 64)
+            lst = np.arange(nb)
+            if pattern == O.TOPK:
+                srow = O.block_scores(O.pool_blocks(qh[r.start:r.stop], 64), kbar)[0]
+                lst, margin = O.topk_row(srow, param)
+            elif pattern == O.FRAME_LOCAL:
+                lst, margin = O.frame_local_row(i, N, T, 64), math.inf
+            if pattern != O.DENSE:
+                gl = idx_h[h, i, :int(cnt_h[h, i])]
+                if np.array_equal(gl, lst):
+                    equal += 1
+                elif pattern == O.TOPK and margin <= 1e-6 and valid_topk(gl, srow, param):
+                    near += 1
+                    lst = gl
+                else:
+                    mismatch += 1
+                    continue
+            ref = O.attend_block(qh, kh, vh, i, lst, 64)[0]
+            err = max(err, float(np.max(np.abs(got[h, r.start:r.stop] - ref))))
+    res = {"workload": name, "dtype": w.dtype, "tokens": N, "key_blocks": nb,
+           "ms_per_step": round(ms_step, 4),
+           "dense_equiv_tflops": round(4 * N * N * 64 * H / (ms_step * 1e-3) / 1e12, 1),
+           "kernels_ms": {"estimate": round(ph[0], 4), "select": round(ph[1], 4),
+                          "attention": round(ph[2], 4)},
+           "achieved_block_sparsity": round(1.0 - kept_pairs / (H * nb * nb), 4),
+           "roofline": {"kernel": "attn_bf16_kernel" if w.dtype == "bf16" else "attn_f32_kernel",
+                        "bound": "mfma", "achieved": round(att_tflops, 2), "peak": peak,
+                        "unit": "TFLOP/s", "frac": round(att_tflops / peak, 4),
+                        "flop_per_launch": flops},
+           "parity": {"query_blocks_per_head": len(rows), "lists_equal": equal,
+                      "near_ties_valid_differing": near, "list_mismatches": mismatch,
+                      "max_abs_err": err, "bound": tol}}
+    del tq, tk, tv, out, sel_ws, att_ws
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -447,6 +559,8 @@ def main():
                     help="query blocks per head in the oracle CPU sample (0 = skip)")
     ap.add_argument("--next-rows", type=int, default=1,
                     help="also time the stride, global-probe, cosine and NMSE kernels (0 = skip)")
+    ap.add_argument("--other-configs", default="S4xT261-f32,S8xT1374-bf16,S32xT1374-bf16",
+                    help="comma-separated smaller workloads also timed and checked (empty = none)")
     ap.add_argument("--split", type=int, default=1, choices=(0, 1),
                     help="1: pass the attention workspace, so lists of 384+ key blocks (on layers of 4096+ "
                          "key blocks) run split "
@@ -644,6 +758,12 @@ def main():
                          f"select/attention scaled by {nb}/{rows}; {wall:.1f} s of CPU work"}
         log(f"[bench] cpu oracle {cpu}")
 
+    others = []
+    for name in [x for x in args.other_configs.split(",") if x]:
+        others.append(other_config(P, torch, name, steps=max(args.steps, 5), warmup=args.warmup,
+                                   seed=args.seed))
+        log(f"[bench] other config {others[-1]}")
+
     traffic = recorded_traffic(w.name)
     result = {
         "metric": METRIC,
@@ -690,6 +810,7 @@ def main():
             "frac": round(2 * nb * nb * 64 * n_topk / (sel_ms * 1e-3) / 1e12 / PEAK_F64_TFLOPS, 4),
         },
         "dense_baseline": dense,
+        "other_configs": others,
         "next_rows": next_rows,
         "cpu_baseline": cpu,
         "parity_sample": parity,
