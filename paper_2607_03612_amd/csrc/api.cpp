@@ -284,15 +284,33 @@ static int attention_cost(const Shape& s, const saf3r_head_cfg* table, int h, in
   }
 }
 
-// On a layer of at least kSplitMinExtent key blocks, a list head whose list
-// can reach kSplitMinBlocks key blocks runs split into key ranges (bf16
-// only).
-static bool attention_split(const Shape& s, const saf3r_head_cfg* table, int h, int cost) {
+static bool listed_class(int p) {
+  return p == SAF3R_FRAME_LOCAL || p == SAF3R_TOPK || p == SAF3R_ANCHOR ||
+         p == SAF3R_GLOBAL_PROBE || p == SAF3R_COSINE_TOPK;
+}
+
+// Key blocks walked by all query blocks of the list and dense heads (the
+// work of the launch that may split).
+static int64_t listed_work(const Shape& s, const saf3r_head_cfg* table, int fl_len) {
+  int64_t total = 0;
+  for (int h = 0; h < s.heads; ++h) {
+    const int p = table[h].pattern;
+    if (p == SAF3R_DENSE || listed_class(p)) total += (int64_t)s.nb * attention_cost(s, table, h, fl_len);
+  }
+  return total;
+}
+
+// bf16 only. On a layer of at least kSplitMinExtent key blocks, a list head
+// whose list can reach kSplitMinBlocks key blocks runs split into key ranges
+// (locality); and a list or dense head whose items walk at least
+// kBalanceMinBlocks blocks, more than twice the layer's work per wave slot
+// (load balance).
+static bool attention_split(const Shape& s, const saf3r_head_cfg* table, int h, int cost,
+                            int64_t work) {
   const int p = table[h].pattern;
-  const bool listed = p == SAF3R_FRAME_LOCAL || p == SAF3R_TOPK || p == SAF3R_ANCHOR ||
-                      p == SAF3R_GLOBAL_PROBE || p == SAF3R_COSINE_TOPK;
-  return listed && s.dtype == SAF3R_BF16 && s.nb >= saf3r::kSplitMinExtent &&
-         cost >= saf3r::kSplitMinBlocks;
+  if (s.dtype != SAF3R_BF16 || !(listed_class(p) || p == SAF3R_DENSE)) return false;
+  if (listed_class(p) && s.nb >= saf3r::kSplitMinExtent && cost >= saf3r::kSplitMinBlocks) return true;
+  return cost >= saf3r::kBalanceMinBlocks && (int64_t)cost * saf3r::kWaveSlots > 2 * work;
 }
 
 int64_t saf3r_attention_workspace_bytes(const saf3r_problem* problem, const saf3r_head_cfg* table) {
@@ -302,9 +320,10 @@ int64_t saf3r_attention_workspace_bytes(const saf3r_problem* problem, const saf3
   st = check_table(s, table);
   if (st != SAF3R_OK) return st;
   const int fl_len = max_frame_local_len(s);
+  const int64_t work = listed_work(s, table, fl_len);
   int64_t n_split = 0;
   for (int h = 0; h < s.heads; ++h)
-    n_split += attention_split(s, table, h, attention_cost(s, table, h, fl_len)) ? 1 : 0;
+    n_split += attention_split(s, table, h, attention_cost(s, table, h, fl_len), work) ? 1 : 0;
   return n_split * saf3r::kSplitChunks * s.nb * saf3r::kSplitItemBytes;
 }
 
@@ -355,6 +374,7 @@ saf3r_status saf3r_sparse_attention(const saf3r_problem* problem, const saf3r_he
   std::vector<int> item_cost(s.heads, 0);
   std::vector<char> is_split(s.heads, 0);
   const int fl_len = max_frame_local_len(s);
+  const int64_t work = listed_work(s, table, fl_len);
   std::vector<int> listed, strided;
   bool all_dense = true;
   for (int h = 0; h < s.heads; ++h) {
@@ -363,7 +383,7 @@ saf3r_status saf3r_sparse_attention(const saf3r_problem* problem, const saf3r_he
     a.dense[h] = p == SAF3R_DENSE ? 1 : 0;
     sa.stride[h] = p == SAF3R_STRIDE ? table[h].param : 1;
     const int cost = attention_cost(s, table, h, fl_len);
-    is_split[h] = split && attention_split(s, table, h, cost) ? 1 : 0;
+    is_split[h] = split && attention_split(s, table, h, cost, work) ? 1 : 0;
     item_cost[h] = is_split[h] ? (cost + saf3r::kSplitChunks - 1) / saf3r::kSplitChunks : cost;
     if (p == SAF3R_STRIDE) {
       strided.push_back(h);
@@ -380,7 +400,9 @@ saf3r_status saf3r_sparse_attention(const saf3r_problem* problem, const saf3r_he
   ma.nb = s.nb;
   ma.splits = saf3r::kSplitChunks;
   a.heads = (int)listed.size();
-  a.mode = all_dense ? 1 : 0;
+  bool any_split = false;
+  for (int h : listed) any_split = any_split || is_split[h];
+  a.mode = all_dense && !any_split ? 1 : 0;  // split items run in the list mode
   a.unit_start[0] = 0;
   for (size_t i = 0; i < listed.size(); ++i) {
     const int h = listed[i];

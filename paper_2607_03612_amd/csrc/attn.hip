@@ -27,8 +27,10 @@
 //
 // Long lists can run split into key ranges: a work item is then (head, key
 // range c of splits, query block) and walks only its list's entries inside
-// range c, ranges in order within a head, so the waves that run together on
-// an XCD read K and V from one range rather than the head's whole extent.
+// range c (a dense head's item walks every block of the range), ranges in
+// order within a head, so the waves that run together on an XCD read K and V
+// from one range rather than the head's whole extent, and no item of a small
+// layer is much longer than the others.
 // Such an item stores its unnormalised O^T and (running max, row sum) per
 // query in a workspace; attn_merge_kernel combines the ranges of each query
 // block in range order.
@@ -260,22 +262,29 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
   const int64_t nkeys = kMode == kStrided ? (a.n + stride - 1) / stride : a.n;
   int count = kMode == kStrided ? (int)((nkeys + kBlock - 1) / kBlock) : nb;
   if (!dense) count = min(max(cnt[(int64_t)w.h * nb + w.i], 0), a.cap);
+  int dense_lo = 0;  // first key block of a dense head's item
   if constexpr (kMode == kLists) {
-    if (w.chunk >= 0 && !dense) {
-      // this item's key range [jlo, jhi): in an ascending list, the entries
-      // after those below jlo and before the first at or above jhi (any other
-      // list still yields a sub-range of the row)
+    if (w.chunk >= 0) {
+      // this item's key range [jlo, jhi)
       const int jlo = (int)(((int64_t)w.chunk * nb) / a.splits);
       const int jhi = (int)(((int64_t)(w.chunk + 1) * nb) / a.splits);
-      int below_lo = 0, below_hi = 0;
-      for (int base = 0; base < count; base += 64) {
-        const int p = base + lane;
-        const int j = p < count ? list[p] : 0x7fffffff;
-        below_lo += __popcll(__ballot(j < jlo));
-        below_hi += __popcll(__ballot(j < jhi));
+      if (dense) {  // every key block of the range
+        dense_lo = jlo;
+        count = jhi - jlo;
+      } else {
+        // in an ascending list, the entries after those below jlo and
+        // before the first at or above jhi (any other list still yields a
+        // sub-range of the row)
+        int below_lo = 0, below_hi = 0;
+        for (int base = 0; base < count; base += 64) {
+          const int p = base + lane;
+          const int j = p < count ? list[p] : 0x7fffffff;
+          below_lo += __popcll(__ballot(j < jlo));
+          below_hi += __popcll(__ballot(j < jhi));
+        }
+        list += below_lo;
+        count = max(below_hi - below_lo, 0);
       }
-      list += below_lo;
-      count = max(below_hi - below_lo, 0);
     }
   }
 
@@ -308,7 +317,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
   // end of the list refetch that tile into a buffer no later step reads
   auto tile_at = [&](int it) -> int {
     const int c = min(it, count - 1);
-    return dense ? c : list[c];
+    return dense ? dense_lo + c : list[c];
   };
 
   f32x16 o[2][2];  // O^T tiles [head-dim half c][query half tq]

@@ -78,6 +78,13 @@ struct GlobalArgs {
 constexpr int kSplitMinBlocks = 384;
 constexpr int kSplitMinExtent = 4096;
 constexpr int kSplitChunks = 4;
+// Load balance: a bf16 list or dense head whose items walk at least
+// kBalanceMinBlocks key blocks is also split when one item is longer than
+// twice the layer's work spread over the chip's wave slots (256 CUs x 4
+// SIMDs x 2 waves), i.e. when its rows, not the total work, would set the
+// launch's length.
+constexpr int kBalanceMinBlocks = 32;
+constexpr int64_t kWaveSlots = 2048;
 constexpr int64_t kSplitItemBytes = (int64_t)kBlock * kHeadDim * 4 + (int64_t)kBlock * 2 * 4;
 
 struct AttnArgs {

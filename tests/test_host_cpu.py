@@ -84,9 +84,11 @@ def _list_len(pattern, param, n, T, nb):
                                      (2, 131072), (64, 4100)])
 def test_capacity_and_attention_split_match_oracle_lists(frames, T):
     """The library's index capacity (longest list over list heads) and the
-    attention split (on layers of 4096 or more key blocks, bf16 list heads
-    whose lists can hold 384 or more key blocks, 4 key ranges of nb items
-    each) against list lengths from the oracle's class definitions, on
+    attention split (bf16 only, 4 key ranges of nb items each: on layers of
+    4096 or more key blocks, list heads whose lists can hold 384 or more key
+    blocks; and list or dense heads walking at least 32 blocks per query
+    block, more than twice the layer's list-and-dense work over 2048 wave
+    slots) against list lengths from the oracle's class definitions, on
     seeded random tables."""
     import ctypes
 
@@ -110,6 +112,12 @@ def test_capacity_and_attention_split_match_oracle_lists(frames, T):
             p = B.problem(len(table), frames, T, dtype)
             t = B.head_table(table)
             assert lib.saf3r_index_capacity(ctypes.byref(p), t) == max(lens + [1]), (table, lens)
-            split = dtype == B.BF16 and nb >= 4096
-            want = 4 * nb * 16896 * sum(1 for x in lens if x >= 384) if split else 0
+            n_dense = sum(1 for c, _ in table if c == B.DENSE)
+            work = nb * (sum(lens) + n_dense * nb)
+
+            def splits(cost, listed):
+                return (listed and nb >= 4096 and cost >= 384) or (cost >= 32 and cost * 2048 > 2 * work)
+
+            n_split = sum(1 for x in lens if splits(x, True)) + n_dense * splits(nb, False)
+            want = 4 * nb * 16896 * n_split if dtype == B.BF16 else 0
             assert lib.saf3r_attention_workspace_bytes(ctypes.byref(p), t) == want, (table, lens)
