@@ -218,13 +218,13 @@ int64_t saf3r_select_workspace_bytes(const saf3r_problem* problem, const saf3r_h
  *                device buffer (16-byte aligned, workspace_bytes >= 0, else
  *                SAF3R_ERR_INVALID_ARGUMENT) of at least
  *                saf3r_attention_workspace_bytes(problem, table) bytes
- *                (else SAF3R_ERR_CAPACITY): bf16 heads of two kinds run as
- *                4 items per query block, one per quarter of the key range
- *                (for L2 locality on long layers: on layers of 4096 or more
- *                key blocks, list heads whose list can hold 384 or more key
- *                blocks; for load balance: list or dense heads whose query
- *                blocks walk at least 32 key blocks, more than twice the
- *                key blocks that all list and dense heads' query blocks
+ *                (else SAF3R_ERR_CAPACITY): heads of two kinds run as 4 items
+ *                per query block, one per quarter of the key range (for L2
+ *                locality, bf16 only: on layers of 4096 or more key blocks,
+ *                list heads whose list can hold 384 or more key blocks; for
+ *                load balance: list or dense heads whose query blocks walk
+ *                at least 32 (bf16) or 8 (fp32) key blocks, more than twice
+ *                the key blocks that all list and dense heads' query blocks
  *                walk, divided by 2048 wave slots), and a second launch merges
  *                the 4 partial softmax results per query in a fixed order
  *                (results differ from the unsplit launch only by fp32
@@ -240,8 +240,8 @@ saf3r_status saf3r_sparse_attention(const saf3r_problem* problem, const saf3r_he
                                     int64_t workspace_bytes, void* stream);
 
 /* Workspace of saf3r_sparse_attention that splits its long lists:
- * (split heads) x 4 x nb x 16896 bytes, where the split heads are the bf16
- * heads saf3r_sparse_attention describes: on a layer of nb >= 4096 key
+ * (split heads) x 4 x nb x 16896 bytes, where the split heads are the heads
+ * saf3r_sparse_attention describes: on a bf16 layer of nb >= 4096 key
  * blocks, the FRAME_LOCAL / TOPK / ANCHOR / GLOBAL_PROBE / COSINE_TOPK heads
  * whose list can hold 384 or more key blocks (2.9 GB for 10 such heads at
  * nb = 4294); and on any layer, list or DENSE heads whose rows are long

@@ -300,17 +300,20 @@ static int64_t listed_work(const Shape& s, const saf3r_head_cfg* table, int fl_l
   return total;
 }
 
-// bf16 only. On a layer of at least kSplitMinExtent key blocks, a list head
-// whose list can reach kSplitMinBlocks key blocks runs split into key ranges
-// (locality); and a list or dense head whose items walk at least
-// kBalanceMinBlocks blocks, more than twice the layer's work per wave slot
-// (load balance).
+// A list or dense head runs split into key ranges: (bf16, locality) on a
+// layer of at least kSplitMinExtent key blocks when its list can reach
+// kSplitMinBlocks key blocks; (load balance, both dtypes) when its items walk
+// at least kBalanceMinBlocks (bf16) or kBalanceMinBlocksF32 (fp32) blocks,
+// more than twice the layer's work per wave slot.
 static bool attention_split(const Shape& s, const saf3r_head_cfg* table, int h, int cost,
                             int64_t work) {
   const int p = table[h].pattern;
-  if (s.dtype != SAF3R_BF16 || !(listed_class(p) || p == SAF3R_DENSE)) return false;
-  if (listed_class(p) && s.nb >= saf3r::kSplitMinExtent && cost >= saf3r::kSplitMinBlocks) return true;
-  return cost >= saf3r::kBalanceMinBlocks && (int64_t)cost * saf3r::kWaveSlots > 2 * work;
+  if (!(listed_class(p) || p == SAF3R_DENSE)) return false;
+  const bool bf16 = s.dtype == SAF3R_BF16;
+  if (bf16 && listed_class(p) && s.nb >= saf3r::kSplitMinExtent && cost >= saf3r::kSplitMinBlocks)
+    return true;
+  const int min_blocks = bf16 ? saf3r::kBalanceMinBlocks : saf3r::kBalanceMinBlocksF32;
+  return cost >= min_blocks && (int64_t)cost * saf3r::kWaveSlots > 2 * work;
 }
 
 int64_t saf3r_attention_workspace_bytes(const saf3r_problem* problem, const saf3r_head_cfg* table) {
@@ -399,6 +402,7 @@ saf3r_status saf3r_sparse_attention(const saf3r_problem* problem, const saf3r_he
   ma.n = s.n;
   ma.nb = s.nb;
   ma.splits = saf3r::kSplitChunks;
+  ma.dtype = s.dtype;
   a.heads = (int)listed.size();
   bool any_split = false;
   for (int h : listed) any_split = any_split || is_split[h];

@@ -101,6 +101,90 @@ __device__ inline Work work_item(const AttnArgs& a) {
   return w;
 }
 
+// A split item's share of its row: key blocks [c nb / splits, (c + 1) nb /
+// splits) of range c. A dense head's item walks every block of the range
+// (from dense_lo); a list head's item keeps its list's entries inside the
+// range: in an ascending list, the entries after those below jlo and before
+// the first at or above jhi (any other list still yields a sub-range of the
+// row, read within it).
+__device__ inline void split_range(const Work& w, const AttnArgs& a, bool dense,
+                                   const int32_t*& list, int& count, int& dense_lo, int lane) {
+  const int nb = a.nb;
+  const int jlo = (int)(((int64_t)w.chunk * nb) / a.splits);
+  const int jhi = (int)(((int64_t)(w.chunk + 1) * nb) / a.splits);
+  if (dense) {
+    dense_lo = jlo;
+    count = jhi - jlo;
+    return;
+  }
+  int below_lo = 0, below_hi = 0;
+  for (int base = 0; base < count; base += 64) {
+    const int p = base + lane;
+    const int j = p < count ? list[p] : 0x7fffffff;
+    below_lo += __popcll(__ballot(j < jlo));
+    below_hi += __popcll(__ballot(j < jhi));
+  }
+  list += below_lo;
+  count = max(below_hi - below_lo, 0);
+}
+
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+
+// A split item's result: its O^T accumulators as they stand, relative to its
+// own running max (register-major: 16 stores of 64 lanes x 16 B), and the
+// (running max, row sum) of each query. An empty range writes only the
+// statistics (-inf, 0), and the merge never reads its accumulators.
+template <typename Acc>
+__device__ inline void store_partials(const Acc (&o)[2][2], const float (&m)[2], const float (&lt)[2],
+                                      const AttnArgs& a, int64_t item, bool empty, int lane) {
+  const int l32 = lane & 31;
+  if (!empty) {
+    float* const po = a.part_o + item * (kBlock * kHeadDim);
+#pragma unroll
+    for (int c = 0; c < 2; ++c)
+#pragma unroll
+      for (int tq = 0; tq < 2; ++tq)
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+          *(f32x4_t*)(po + (((c * 2 + tq) * 4 + g) * 64 + lane) * 4) =
+              f32x4_t{o[c][tq][4 * g], o[c][tq][4 * g + 1], o[c][tq][4 * g + 2], o[c][tq][4 * g + 3]};
+  }
+  if ((lane >> 5) == 0) {
+#pragma unroll
+    for (int tq = 0; tq < 2; ++tq)
+      *(f32x2_t*)(a.part_ml + (item * kBlock + 32 * tq + l32) * 2) =
+          empty ? f32x2_t{-__builtin_inff(), 0.f} : f32x2_t{m[tq], lt[tq]};
+  }
+}
+
+// fp32 output of one query block from the O^T accumulators (register e of
+// tile [c][tq] of lane (l32, hf) is head dim 32c + 8(e/4) + 4hf + e%4 of
+// query 32tq + l32), scaled by inv; lse_row, if not null, is the head's LSE
+// row (natural log).
+template <typename Acc>
+__device__ inline void write_out_tile_f32(const Acc (&o)[2][2], const float (&inv)[2],
+                                          const float (&lse_val)[2], __amdgpu_buffer_rsrc_t ro,
+                                          float* lse_row, int i, int64_t n, int lane) {
+  const int l32 = lane & 31;
+  const int hf = lane >> 5;
+#pragma unroll
+  for (int tq = 0; tq < 2; ++tq) {
+    const int query = i * kBlock + 32 * tq + l32;
+#pragma unroll
+    for (int c = 0; c < 2; ++c)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        f32x4_t ov;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) ov[r] = o[c][tq][4 * g + r] * inv[tq];
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(i32x4, ov), ro,
+                                               (query * kHeadDim + 32 * c + 8 * g + 4 * hf) * 4, 0, 0);
+      }
+    if (lse_row && hf == 0 && query < n) lse_row[query] = lse_val[tq];
+  }
+}
+
 // ------------------------------------------------------------------ bf16
 
 typedef __attribute__((address_space(3))) void lds_void;
@@ -264,28 +348,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
   if (!dense) count = min(max(cnt[(int64_t)w.h * nb + w.i], 0), a.cap);
   int dense_lo = 0;  // first key block of a dense head's item
   if constexpr (kMode == kLists) {
-    if (w.chunk >= 0) {
-      // this item's key range [jlo, jhi)
-      const int jlo = (int)(((int64_t)w.chunk * nb) / a.splits);
-      const int jhi = (int)(((int64_t)(w.chunk + 1) * nb) / a.splits);
-      if (dense) {  // every key block of the range
-        dense_lo = jlo;
-        count = jhi - jlo;
-      } else {
-        // in an ascending list, the entries after those below jlo and
-        // before the first at or above jhi (any other list still yields a
-        // sub-range of the row)
-        int below_lo = 0, below_hi = 0;
-        for (int base = 0; base < count; base += 64) {
-          const int p = base + lane;
-          const int j = p < count ? list[p] : 0x7fffffff;
-          below_lo += __popcll(__ballot(j < jlo));
-          below_hi += __popcll(__ballot(j < jhi));
-        }
-        list += below_lo;
-        count = max(below_hi - below_lo, 0);
-      }
-    }
+    if (w.chunk >= 0) split_range(w, a, dense, list, count, dense_lo, lane);
   }
 
   const int64_t head_off = (int64_t)w.h * a.n * kHeadDim;
@@ -333,11 +396,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
   if (count <= 0) {  // an empty list: no keys, zero output, LSE -inf
     if constexpr (kMode == kLists) {
       if (w.chunk >= 0) {  // an empty key range: statistics only, the merge skips it
-        if (hf == 0) {
-#pragma unroll
-          for (int tq = 0; tq < 2; ++tq)
-            *(f32x2*)(a.part_ml + ((int64_t)w.item * kBlock + 32 * tq + l32) * 2) = f32x2{kNegInf, 0.f};
-        }
+        store_partials(o, m, l, a, w.item, true, lane);
         return;
       }
     }
@@ -590,23 +649,8 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
 #pragma unroll
   for (int tq = 0; tq < 2; ++tq) lt[tq] = pair_sum(l[tq]);
   if constexpr (kMode == kLists) {
-    if (w.chunk >= 0) {
-      // a split item: O^T accumulators as they stand (register-major, 1 KB
-      // per store instruction) and (running max, row sum) per query
-      float* const po = a.part_o + (int64_t)w.item * (kBlock * kHeadDim);
-#pragma unroll
-      for (int c = 0; c < 2; ++c)
-#pragma unroll
-        for (int tq = 0; tq < 2; ++tq)
-#pragma unroll
-          for (int g = 0; g < 4; ++g)
-            *(f32x4*)(po + (((c * 2 + tq) * 4 + g) * 64 + lane) * 4) =
-                f32x4{o[c][tq][4 * g], o[c][tq][4 * g + 1], o[c][tq][4 * g + 2], o[c][tq][4 * g + 3]};
-      if (hf == 0) {
-#pragma unroll
-        for (int tq = 0; tq < 2; ++tq)
-          *(f32x2*)(a.part_ml + ((int64_t)w.item * kBlock + 32 * tq + l32) * 2) = f32x2{m[tq], lt[tq]};
-      }
+    if (w.chunk >= 0) {  // a split item: the merge combines the ranges
+      store_partials(o, m, lt, a, w.item, false, lane);
       return;
     }
   }
@@ -618,10 +662,12 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
 
 // Combines the key ranges of split heads: per query, M = max of the ranges'
 // running maxima, weights 2^(m_c - M), O = sum_c w_c O_c / sum_c w_c l_c, in
-// range order. One wave per (split head, query block).
+// range order; rows written in the layer's dtype. One wave per (split head,
+// query block).
+template <bool kBf16>
 __global__ __launch_bounds__(64) void attn_merge_kernel(const float* __restrict__ part_o,
                                                        const float* __restrict__ part_ml,
-                                                       uint16_t* __restrict__ out,
+                                                       void* __restrict__ out,
                                                        float* __restrict__ lse, MergeArgs a) {
   __shared__ __attribute__((aligned(1024))) char b0[32 * 128];
   __shared__ __attribute__((aligned(1024))) char b1[32 * 128];
@@ -676,9 +722,16 @@ __global__ __launch_bounds__(64) void attn_merge_kernel(const float* __restrict_
     lse_val[tq] = lt[tq] > 0.f ? (mx[tq] + __log2f(lt[tq])) * kLn2 : kNegInf;
   }
   const int64_t head_off = (int64_t)h * a.n * kHeadDim;
-  const __amdgpu_buffer_rsrc_t ro = make_rsrc(out + head_off, (uint32_t)(a.n * kHeadDim * 2));
-  write_out_tile(o, inv, lse_val, (lds_char*)b0, (lds_char*)b1, ro,
-                 lse ? lse + (int64_t)h * a.n : nullptr, i, a.n, lane);
+  float* const lse_row = lse ? lse + (int64_t)h * a.n : nullptr;
+  if constexpr (kBf16) {
+    const __amdgpu_buffer_rsrc_t ro =
+        make_rsrc(static_cast<uint16_t*>(out) + head_off, (uint32_t)(a.n * kHeadDim * 2));
+    write_out_tile(o, inv, lse_val, (lds_char*)b0, (lds_char*)b1, ro, lse_row, i, a.n, lane);
+  } else {
+    const __amdgpu_buffer_rsrc_t ro =
+        make_rsrc(static_cast<float*>(out) + head_off, (uint32_t)(a.n * kHeadDim * 4));
+    write_out_tile_f32(o, inv, lse_val, ro, lse_row, i, a.n, lane);
+  }
 }
 
 // ------------------------------------------------------------------ fp32
@@ -708,6 +761,10 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(const float* __restrict__ 
   const int64_t nkeys = kMode == kStrided ? (a.n + stride - 1) / stride : a.n;
   int count = kMode == kStrided ? (int)((nkeys + kBlock - 1) / kBlock) : nb;
   if (!dense) count = min(max(cnt[(int64_t)w.h * nb + w.i], 0), a.cap);
+  int dense_lo = 0;  // first key block of a dense head's item
+  if constexpr (kMode == kLists) {
+    if (w.chunk >= 0) split_range(w, a, dense, list, count, dense_lo, lane);
+  }
   const int last_block = kMode == kStrided ? count - 1 : nb - 1;
 
   const int64_t head_off = (int64_t)w.h * a.n * kHeadDim;
@@ -748,7 +805,7 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(const float* __restrict__ 
   const float sc = a.scale_log2;
 
   for (int it = 0; it < count; ++it) {
-    const int j = dense ? it : list[it];
+    const int j = dense ? dense_lo + it : list[it];
     // stage K and V tiles: rows 4n + lane/16, float4 chunk lane%16 (a STRIDE
     // head's row r of virtual block j is token (64j + r) * stride; tokens at
     // or past n read as zeros through an offset past the buffer's extent)
@@ -836,24 +893,23 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(const float* __restrict__ 
         }
   }
 
+  float lt[2];
+#pragma unroll
+  for (int tq = 0; tq < 2; ++tq) lt[tq] = l[tq] + __shfl_xor(l[tq], 32);
+  if constexpr (kMode == kLists) {
+    if (w.chunk >= 0) {  // a split item: the merge combines the ranges
+      store_partials(o, m, lt, a, w.item, count <= 0, lane);
+      return;
+    }
+  }
+  // an empty list (no keys) gives a zero output and LSE -inf
+  float inv[2], lse_val[2];
 #pragma unroll
   for (int tq = 0; tq < 2; ++tq) {
-    const float lt = l[tq] + __shfl_xor(l[tq], 32);
-    const float inv = 1.0f / lt;
-    const int query = w.i * kBlock + 32 * tq + l32;
-#pragma unroll
-    for (int c = 0; c < 2; ++c)
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        f32x4 ov;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) ov[r] = o[c][tq][4 * g + r] * inv;
-        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(i32x4, ov), ro,
-                                               (query * kHeadDim + 32 * c + 8 * g + 4 * hf) * 4, 0, 0);
-      }
-    if (lse && hf == 0 && query < a.n)
-      lse[(int64_t)w.h * a.n + query] = (m[tq] + log2f(lt)) * kLn2;
+    inv[tq] = lt[tq] > 0.f ? 1.0f / lt[tq] : 0.f;
+    lse_val[tq] = lt[tq] > 0.f ? (m[tq] + log2f(lt[tq])) * kLn2 : kNegInf;
   }
+  write_out_tile_f32(o, inv, lse_val, ro, lse ? lse + (int64_t)w.h * a.n : nullptr, w.i, a.n, lane);
 }
 
 }  // namespace
@@ -883,8 +939,12 @@ hipError_t launch_attention_merge(const float* part_o, const float* part_ml, voi
                                   float* lse, const MergeArgs& a, hipStream_t s) {
   const int64_t groups = (int64_t)a.n_split * a.nb;
   if (groups == 0) return hipSuccess;
-  hipLaunchKernelGGL(attn_merge_kernel, dim3((unsigned)groups), dim3(64), 0, s, part_o, part_ml,
-                     static_cast<uint16_t*>(out), lse, a);
+  if (a.dtype == 1)
+    hipLaunchKernelGGL(attn_merge_kernel<true>, dim3((unsigned)groups), dim3(64), 0, s, part_o,
+                       part_ml, out, lse, a);
+  else
+    hipLaunchKernelGGL(attn_merge_kernel<false>, dim3((unsigned)groups), dim3(64), 0, s, part_o,
+                       part_ml, out, lse, a);
   return hipGetLastError();
 }
 

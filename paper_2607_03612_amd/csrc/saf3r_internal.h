@@ -78,12 +78,15 @@ struct GlobalArgs {
 constexpr int kSplitMinBlocks = 384;
 constexpr int kSplitMinExtent = 4096;
 constexpr int kSplitChunks = 4;
-// Load balance: a bf16 list or dense head whose items walk at least
-// kBalanceMinBlocks key blocks is also split when one item is longer than
-// twice the layer's work spread over the chip's wave slots (256 CUs x 4
-// SIMDs x 2 waves), i.e. when its rows, not the total work, would set the
-// launch's length.
+// Load balance: a list or dense head whose items walk at least
+// kBalanceMinBlocks (bf16) or kBalanceMinBlocksF32 key blocks is also split
+// when one item is longer than twice the layer's work spread over the chip's
+// wave slots (256 CUs x 4 SIMDs x 2 waves), i.e. when its rows, not the total
+// work, would set the launch's length. An fp32 tile costs about eight times
+// a bf16 one (fp32 matrix cores, one wave per SIMD), so shorter fp32 rows
+// are worth splitting.
 constexpr int kBalanceMinBlocks = 32;
+constexpr int kBalanceMinBlocksF32 = 8;
 constexpr int64_t kWaveSlots = 2048;
 constexpr int64_t kSplitItemBytes = (int64_t)kBlock * kHeadDim * 4 + (int64_t)kBlock * 2 * 4;
 
@@ -111,6 +114,7 @@ struct MergeArgs {
   int32_t nb;
   int32_t splits;
   int32_t n_split;
+  int32_t dtype;  // of the output rows: 1 bf16, 0 fp32
   int16_t head[kMaxHeads];  // by split index: head
 };
 

@@ -122,6 +122,7 @@ hipError_t launch_attention(int dtype, const void* q, const void* k, const void*
 hipError_t launch_attention_merge(const float* part_o, const float* part_ml, void* out, float*,
                                   const MergeArgs& a, hipStream_t) {
   return verdict(part_o && part_ml && out && blocks_ok(a.n, a.nb) && a.splits == kSplitChunks &&
+                 (a.dtype == 0 || a.dtype == 1) &&
                  heads_ok(a.head, a.n_split, kMaxHeads) && a.n_split >= 1 &&
                  part_ml == part_o + (int64_t)a.n_split * a.splits * a.nb * kBlock * kHeadDim);
 }

@@ -84,12 +84,12 @@ def _list_len(pattern, param, n, T, nb):
                                      (2, 131072), (64, 4100)])
 def test_capacity_and_attention_split_match_oracle_lists(frames, T):
     """The library's index capacity (longest list over list heads) and the
-    attention split (bf16 only, 4 key ranges of nb items each: on layers of
+    attention split (4 key ranges of nb items each: for bf16 on layers of
     4096 or more key blocks, list heads whose lists can hold 384 or more key
-    blocks; and list or dense heads walking at least 32 blocks per query
-    block, more than twice the layer's list-and-dense work over 2048 wave
-    slots) against list lengths from the oracle's class definitions, on
-    seeded random tables."""
+    blocks; and list or dense heads walking at least 32 (bf16) or 8 (fp32)
+    blocks per query block, more than twice the layer's list-and-dense work
+    over 2048 wave slots) against list lengths from the oracle's class
+    definitions, on seeded random tables."""
     import ctypes
 
     lib = B.load()
@@ -116,8 +116,10 @@ def test_capacity_and_attention_split_match_oracle_lists(frames, T):
             work = nb * (sum(lens) + n_dense * nb)
 
             def splits(cost, listed):
-                return (listed and nb >= 4096 and cost >= 384) or (cost >= 32 and cost * 2048 > 2 * work)
+                bf16 = dtype == B.BF16
+                return (bf16 and listed and nb >= 4096 and cost >= 384) or \
+                    (cost >= (32 if bf16 else 8) and cost * 2048 > 2 * work)
 
             n_split = sum(1 for x in lens if splits(x, True)) + n_dense * splits(nb, False)
-            want = 4 * nb * 16896 * n_split if dtype == B.BF16 else 0
+            want = 4 * nb * 16896 * n_split
             assert lib.saf3r_attention_workspace_bytes(ctypes.byref(p), t) == want, (table, lens)
