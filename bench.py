@@ -8,8 +8,9 @@ table with 6 frame-local and 10 Top-K heads (target block sparsity 95%).
 
 Prints one JSON line: dense-equivalent TFLOP/s (4 N^2 64 H per layer over
 the measured step time) with ms per step, the attention kernel's roofline,
-the estimation kernel's HBM rate, the dense baseline from the same kernel,
-and the CPU oracle timed on a bounded sample of the same workload.
+the estimation kernel's HBM rate, the dense baseline (every head dense: the
+shared-tile dense kernel) and the CPU oracle timed on a bounded sample of the
+same workload.
 """
 from __future__ import annotations
 
@@ -682,7 +683,7 @@ def main():
     log(f"[bench] step {ms_step:.3f} ms (estimate {est_ms:.3f}, select {sel_ms:.3f}, "
         f"attention {att_ms:.3f}); sparsity {sparsity:.4f}; attention {att_tflops:.1f} TFLOP/s")
 
-    # dense baseline: the same attention kernel with every head dense
+    # dense baseline: every head dense (the library's all-dense kernel)
     dense_tab = [(0, 0)] * H
     dense = None
     if args.dense_reps > 0:

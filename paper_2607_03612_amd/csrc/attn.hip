@@ -34,6 +34,11 @@
 // Such an item stores its unnormalised O^T and (running max, row sum) per
 // query in a workspace; attn_merge_kernel combines the ranges of each query
 // block in range order.
+//
+// A launch in which every head is dense runs attn_bf16_dense_kernel: four
+// waves take four neighbouring query blocks of one head, and since all four
+// walk every key block in order, each K and V half tile is staged in LDS
+// once for the four (one barrier per half-tile step).
 #include <type_traits>
 
 #include "saf3r_internal.h"
@@ -313,6 +318,224 @@ __device__ inline void write_out_tile(const f32x16 (&o)[2][2], const float (&inv
   }
 }
 
+// Per-wave state and building blocks of the bf16 walk over one 64-query
+// block: Q^T in registers, the O^T accumulators, the running max and row-sum
+// share of each query half, and the lane's LDS operand offsets.
+template <bool kPin>
+struct Bf16Walk {
+  bf16x8 qB[2][4];  // Q^T as the B operand: qB[tq][s] = Q[64i + 32tq + l32][16s + 8hf + (0..7)]
+  f32x16 o[2][2];   // O^T tiles [head-dim half c][query half tq]
+  float m[2];       // running max of the log2-scaled scores
+  float l[2];       // this lane's share of the running row sum
+  float sc;
+  int l32, hf;
+  int tr_row, tr_col;  // transposing-read position of this lane in a 4-row x 16-column group
+  // Lane parts of the LDS operand addresses: the K read of chunk pair st (row
+  // l32), and the transposing V reads of column half c, rows +0 / +8 of a
+  // 16-row group (the 16-row group's 2 KB is an immediate offset). With kPin
+  // an empty asm redefines a part at each use, so the buffer's base also
+  // goes into the immediate offset instead of one hoisted address register
+  // per (buffer, part): eight registers in all for a ring of eight buffers.
+  // With two buffers per tensor the hoisted addresses measured faster.
+  int kpart[4];
+  int vpart[2][2];
+
+  __device__ __forceinline__ void init(__amdgpu_buffer_rsrc_t rq, int i, int lane, float scale) {
+    l32 = lane & 31;
+    hf = lane >> 5;
+    sc = scale;
+#pragma unroll
+    for (int tq = 0; tq < 2; ++tq)
+#pragma unroll
+      for (int s = 0; s < 4; ++s)
+        qB[tq][s] = load_b128(
+            rq, (uint32_t)(((i * kBlock + 32 * tq + l32) * kHeadDim + 16 * s + 8 * hf) * 2));
+#pragma unroll
+    for (int c = 0; c < 2; ++c)
+#pragma unroll
+      for (int tq = 0; tq < 2; ++tq)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) o[c][tq][e] = 0.f;
+    m[0] = m[1] = kNegInf;
+    l[0] = l[1] = 0.f;
+    tr_row = 4 * hf + ((lane & 15) >> 2);
+    tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+#pragma unroll
+    for (int st = 0; st < 4; ++st) kpart[st] = swz(l32, 2 * st + hf);
+#pragma unroll
+    for (int c = 0; c < 2; ++c)
+#pragma unroll
+      for (int r8 = 0; r8 < 2; ++r8)
+        vpart[c][r8] = swz(tr_row + 8 * r8, (32 * c + tr_col) >> 3) + (tr_col & 7) * 2;
+  }
+
+  // S^T of a key half (32 keys x 64 queries) from an LDS K half buffer
+  __device__ __forceinline__ void read_k(lds_char* kb, bf16x8 (&kA)[4]) {
+#pragma unroll
+    for (int st = 0; st < 4; ++st) {
+      if constexpr (kPin) asm volatile("" : "+v"(kpart[st]));
+      kA[st] = *(lds_bf16x8*)(kb + kpart[st]);
+    }
+  }
+  __device__ __forceinline__ void read_v(lds_char* vb, bf16x8 (&vA)[2][2]) {
+    if constexpr (kPin) {
+#pragma unroll
+      for (int c = 0; c < 2; ++c)
+#pragma unroll
+        for (int r8 = 0; r8 < 2; ++r8) asm volatile("" : "+v"(vpart[c][r8]));
+    }
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int c = 0; c < 2; ++c) {
+        const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vb + 2048 * u + vpart[c][0]));
+        const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vb + 2048 * u + vpart[c][1]));
+        vA[u][c] = bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+      }
+  }
+  __device__ __forceinline__ void mfma_s(const bf16x8 (&kA)[4], f32x16 (&s)[2]) {
+    f32x16 acc0 = {}, acc1 = {};
+#pragma unroll
+    for (int st = 0; st < 4; ++st) {
+      acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kA[st], qB[0][st], acc0, 0, 0, 0);
+      acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kA[st], qB[1][st], acc1, 0, 0, 0);
+    }
+    s[0] = acc0;
+    s[1] = acc1;
+  }
+  __device__ __forceinline__ void mfma_pv(const bf16x8 (&vA)[2][2], const bf16x8 (&p)[2][2]) {
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int c = 0; c < 2; ++c)
+#pragma unroll
+        for (int tq = 0; tq < 2; ++tq)
+          o[c][tq] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vA[u][c], p[u][tq], o[c][tq], 0, 0, 0);
+  }
+  // Online-softmax step over one key half. P = exp2(s*sc - m) is taken with
+  // the running max as it stands and rounded to bf16; the row sum adds the
+  // rounded values (one bf16 dot with (1, 1) per pair), so the normaliser
+  // matches the weights the P V product uses. Only when some lane's share of
+  // the row sum leaves [0, 2^12] (a new larger max, or the first half where
+  // the max is still -inf and the sum is inf or NaN) is the half's max taken:
+  // the running max moves to it, O and l are rescaled (after the P V of the
+  // previous half, which is already issued) and P is recomputed. Keys at or
+  // past `valid` (a partial last block) get P = 0.
+  __device__ __forceinline__ void probs(const f32x16 (&s)[2], bf16x8 (&p)[2][2], float (&rs)[2]) {
+#pragma unroll
+    for (int tq = 0; tq < 2; ++tq) {
+      const float mcur = m[tq];
+      float r = 0.f;
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        bf16x2 pr[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const f32x2 pf = {fast_exp2(fmaf(s[tq][8 * u + 2 * e], sc, -mcur)),
+                            fast_exp2(fmaf(s[tq][8 * u + 2 * e + 1], sc, -mcur))};
+          pr[e] = __builtin_convertvector(pf, bf16x2);
+          r = __builtin_amdgcn_fdot2_f32_bf16(pr[e], kOnes, r, false);
+        }
+        p[u][tq] = bf16x8{pr[0][0], pr[0][1], pr[1][0], pr[1][1],
+                          pr[2][0], pr[2][1], pr[3][0], pr[3][1]};
+      }
+      rs[tq] = r;
+    }
+  }
+  __device__ __forceinline__ void mask_keys(f32x16 (&s)[2], int valid) {
+    if (valid < 32) {
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int key = 8 * (e >> 2) + 4 * hf + (e & 3);
+        if (key >= valid) {
+          s[0][e] = kNegInf;
+          s[1][e] = kNegInf;
+        }
+      }
+    }
+  }
+  __device__ __forceinline__ void fixup(f32x16 (&s)[2], bf16x8 (&p)[2][2], float (&rs)[2]) {
+    // 0x45800000 is 2^12; inf and NaN compare above it as unsigned bits
+    if (__ballot(__float_as_uint(rs[0]) > 0x45800000u || __float_as_uint(rs[1]) > 0x45800000u)) {
+#pragma unroll
+      for (int tq = 0; tq < 2; ++tq) {
+        float mx = fmaxf(fmaxf(s[tq][0], s[tq][1]), s[tq][2]);
+#pragma unroll
+        for (int e = 3; e < 15; e += 2) mx = fmaxf(fmaxf(mx, s[tq][e]), s[tq][e + 1]);
+        mx = fmaxf(mx, s[tq][15]);
+        const float mnew = fmaxf(pair_max(mx) * sc, m[tq]);
+        const float alpha = fast_exp2(m[tq] - mnew);
+        m[tq] = mnew;
+        l[tq] *= alpha;
+#pragma unroll
+        for (int c = 0; c < 2; ++c) o[c][tq] *= alpha;
+      }
+      probs(s, p, rs);
+    }
+    l[0] += rs[0];
+    l[1] += rs[1];
+  }
+
+  // One half-tile step t: Sᵀ of half t+1 (from kb, if kNext) and O += Vᵀ Pᵀ
+  // of half t-1 (from vb) on the matrix cores while the VALU runs the softmax
+  // of half t (s_cur, keys past `valid` masked); then s_cur and p_prev move
+  // on by one half. Both are issued in one scheduling region: the 12 LDS
+  // operand reads first (mask 0x100), ten softmax VALU ops (0x002) while they
+  // land, then each of the 16 MFMAs (0x008) followed by four VALU ops, so the
+  // matrix cores and the VALU work on independent data side by side.
+  template <bool kNext>
+  __device__ __forceinline__ void step(lds_char* kb, lds_char* vb, int valid, f32x16 (&s_cur)[2],
+                       bf16x8 (&p_prev)[2][2]) {
+    bf16x8 kA[4];
+    bf16x8 vA[2][2];
+    if constexpr (kNext) read_k(kb, kA);
+    read_v(vb, vA);
+    f32x16 s_next[2];
+    if constexpr (kNext) mfma_s(kA, s_next);
+    mfma_pv(vA, p_prev);
+    bf16x8 p_new[2][2];
+    mask_keys(s_cur, valid);
+    float rs[2];
+    probs(s_cur, p_new, rs);
+    __builtin_amdgcn_sched_group_barrier(0x100, 12, 0);
+    __builtin_amdgcn_sched_group_barrier(0x002, 10, 0);
+#pragma unroll
+    for (int g = 0; g < 16; ++g) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
+    }
+    fixup(s_cur, p_new, rs);
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int tq = 0; tq < 2; ++tq) p_prev[u][tq] = p_new[u][tq];
+    if constexpr (kNext) {
+      s_cur[0] = s_next[0];
+      s_cur[1] = s_next[1];
+    }
+  }
+  // The last step: no half t+1; O += Vᵀ Pᵀ of half t-1, the softmax of half
+  // t, then the P V of half t itself.
+  __device__ __forceinline__ void last_step(lds_char* vb_prev, lds_char* vb_cur, int valid, f32x16 (&s_cur)[2],
+                            const bf16x8 (&p_prev)[2][2]) {
+    bf16x8 vA[2][2];
+    read_v(vb_prev, vA);
+    mfma_pv(vA, p_prev);
+    bf16x8 p_new[2][2];
+    mask_keys(s_cur, valid);
+    float rs[2];
+    probs(s_cur, p_new, rs);
+    fixup(s_cur, p_new, rs);
+    read_v(vb_cur, vA);
+    mfma_pv(vA, p_new);
+  }
+  // the row sums of the two query halves (the lane pair's shares added)
+  __device__ __forceinline__ void row_sums(float (&lt)[2]) const {
+    lt[0] = pair_sum(l[0]);
+    lt[1] = pair_sum(l[1]);
+  }
+};
+
 template <int kMode>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_bf16_kernel(const uint16_t* __restrict__ q,
                                                       const uint16_t* __restrict__ k,
@@ -353,7 +576,6 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
 
   const int64_t head_off = (int64_t)w.h * a.n * kHeadDim;
   const uint32_t head_bytes = (uint32_t)(a.n * kHeadDim * 2);
-  const __amdgpu_buffer_rsrc_t rq = make_rsrc(q + head_off, head_bytes);
   const __amdgpu_buffer_rsrc_t rk = make_rsrc(k + head_off, head_bytes);
   const __amdgpu_buffer_rsrc_t rv = make_rsrc(v + head_off, head_bytes);
   const __amdgpu_buffer_rsrc_t ro = make_rsrc(out + head_off, head_bytes);
@@ -366,14 +588,8 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
       dma_half(is_v ? vh : kh, head_bytes, nb, j, h, buf, off);
   };
 
-  // Q^T as the B operand: qB[tq][s] = Q[64i + 32tq + l32][16s + 8hf + (0..7)]
-  bf16x8 qB[2][4];
-#pragma unroll
-  for (int tq = 0; tq < 2; ++tq)
-#pragma unroll
-    for (int s = 0; s < 4; ++s)
-      qB[tq][s] = load_b128(
-          rq, (uint32_t)(((w.i * kBlock + 32 * tq + l32) * kHeadDim + 16 * s + 8 * hf) * 2));
+  Bf16Walk<false> wk;
+  wk.init(make_rsrc(q + head_off, head_bytes), w.i, lane, a.scale_log2);
 
   const DmaLaneOffsets dma_off = dma_lane_offset(lane);
   // tile of list position it, clamped to the last kept tile: loads past the
@@ -383,20 +599,10 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
     return dense ? dense_lo + c : list[c];
   };
 
-  f32x16 o[2][2];  // O^T tiles [head-dim half c][query half tq]
-#pragma unroll
-  for (int c = 0; c < 2; ++c)
-#pragma unroll
-    for (int tq = 0; tq < 2; ++tq)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) o[c][tq][e] = 0.f;
-  float m[2] = {kNegInf, kNegInf};  // running max of the log2-scaled scores
-  float l[2] = {0.f, 0.f};          // this lane's share of the running row sum
-
   if (count <= 0) {  // an empty list: no keys, zero output, LSE -inf
     if constexpr (kMode == kLists) {
       if (w.chunk >= 0) {  // an empty key range: statistics only, the merge skips it
-        store_partials(o, m, l, a, w.item, true, lane);
+        store_partials(wk.o, wk.m, wk.l, a, w.item, true, lane);
         return;
       }
     }
@@ -418,128 +624,13 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
   const int last_block = kMode == kStrided ? count - 1 : nb - 1;
   const bool tail = (nkeys % kBlock) != 0;
   const int valid_last = (int)(nkeys - (int64_t)last_block * kBlock);
-  const float sc = a.scale_log2;
-  // transposing-read position of this lane inside a 4-row x 16-column group
-  const int tr_row = 4 * hf + ((lane & 15) >> 2);
-  const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
-
-  // ---- building blocks of one half-tile step
-
-  // S^T of a key half (32 keys x 64 queries) from an LDS K half buffer
-  auto read_k = [&](lds_char* kb, bf16x8 (&kA)[4]) {
-#pragma unroll
-    for (int st = 0; st < 4; ++st) kA[st] = *(lds_bf16x8*)(kb + swz(l32, 2 * st + hf));
-  };
-  auto read_v = [&](lds_char* vb, bf16x8 (&vA)[2][2]) {
-#pragma unroll
-    for (int u = 0; u < 2; ++u)
-#pragma unroll
-      for (int c = 0; c < 2; ++c) {
-        const int krow = 16 * u + tr_row;
-        const int col = 32 * c + tr_col;
-        const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
-            (lds_bf16x4*)(vb + swz(krow, col >> 3) + (col & 7) * 2));
-        const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
-            (lds_bf16x4*)(vb + swz(krow + 8, col >> 3) + (col & 7) * 2));
-        vA[u][c] = bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-      }
-  };
-  auto mfma_s = [&](const bf16x8 (&kA)[4], f32x16 (&s)[2]) {
-    f32x16 acc0 = {}, acc1 = {};
-#pragma unroll
-    for (int st = 0; st < 4; ++st) {
-      acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kA[st], qB[0][st], acc0, 0, 0, 0);
-      acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kA[st], qB[1][st], acc1, 0, 0, 0);
-    }
-    s[0] = acc0;
-    s[1] = acc1;
-  };
-  auto mfma_pv = [&](const bf16x8 (&vA)[2][2], const bf16x8 (&p)[2][2]) {
-#pragma unroll
-    for (int u = 0; u < 2; ++u)
-#pragma unroll
-      for (int c = 0; c < 2; ++c)
-#pragma unroll
-        for (int tq = 0; tq < 2; ++tq)
-          o[c][tq] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vA[u][c], p[u][tq], o[c][tq], 0, 0, 0);
-  };
-  // Online-softmax step over one key half. P = exp2(s*sc - m) is taken with
-  // the running max as it stands and rounded to bf16; the row sum adds the
-  // rounded values (one bf16 dot with (1, 1) per pair), so the normaliser
-  // matches the weights the P V product uses. Only when some lane's share of
-  // the row sum leaves [0, 2^12] (a new larger max, or the first half where
-  // the max is still -inf and the sum is inf or NaN) is the half's max taken:
-  // the running max moves to it, O and l are rescaled (after the P V of the
-  // previous half, which is already issued) and P is recomputed. Keys at or
-  // past `valid` (a partial last block) get P = 0.
-  auto probs = [&](const f32x16 (&s)[2], bf16x8 (&p)[2][2], float (&rs)[2]) {
-#pragma unroll
-    for (int tq = 0; tq < 2; ++tq) {
-      const float mcur = m[tq];
-      float r = 0.f;
-#pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        bf16x2 pr[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const f32x2 pf = {fast_exp2(fmaf(s[tq][8 * u + 2 * e], sc, -mcur)),
-                            fast_exp2(fmaf(s[tq][8 * u + 2 * e + 1], sc, -mcur))};
-          pr[e] = __builtin_convertvector(pf, bf16x2);
-          r = __builtin_amdgcn_fdot2_f32_bf16(pr[e], kOnes, r, false);
-        }
-        p[u][tq] = bf16x8{pr[0][0], pr[0][1], pr[1][0], pr[1][1],
-                          pr[2][0], pr[2][1], pr[3][0], pr[3][1]};
-      }
-      rs[tq] = r;
-    }
-  };
-  auto mask_keys = [&](f32x16 (&s)[2], int valid) {
-    if (valid < 32) {
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int key = 8 * (e >> 2) + 4 * hf + (e & 3);
-        if (key >= valid) {
-          s[0][e] = kNegInf;
-          s[1][e] = kNegInf;
-        }
-      }
-    }
-  };
-  auto fixup = [&](f32x16 (&s)[2], bf16x8 (&p)[2][2], float (&rs)[2]) {
-    // 0x45800000 is 2^12; inf and NaN compare above it as unsigned bits
-    if (__ballot(__float_as_uint(rs[0]) > 0x45800000u || __float_as_uint(rs[1]) > 0x45800000u)) {
-#pragma unroll
-      for (int tq = 0; tq < 2; ++tq) {
-        float mx = fmaxf(fmaxf(s[tq][0], s[tq][1]), s[tq][2]);
-#pragma unroll
-        for (int e = 3; e < 15; e += 2) mx = fmaxf(fmaxf(mx, s[tq][e]), s[tq][e + 1]);
-        mx = fmaxf(mx, s[tq][15]);
-        const float mnew = fmaxf(pair_max(mx) * sc, m[tq]);
-        const float alpha = fast_exp2(m[tq] - mnew);
-        m[tq] = mnew;
-        l[tq] *= alpha;
-#pragma unroll
-        for (int c = 0; c < 2; ++c) o[c][tq] *= alpha;
-      }
-      probs(s, p, rs);
-    }
-    l[0] += rs[0];
-    l[1] += rs[1];
-  };
-  auto softmax = [&](f32x16 (&s)[2], int valid, bf16x8 (&p)[2][2]) {
-    mask_keys(s, valid);
-    float rs[2];
-    probs(s, p, rs);
-    fixup(s, p, rs);
-  };
 
   // ---- pipeline
   // Half-tile steps t = 2j + h (tile j of the list, key half h). Step t
-  // issues S^T of half t+1 and O += V^T P^T of half t-1 on the matrix cores
-  // while the VALU runs the softmax of half t, then refills the buffers it
-  // read: K half t+3 (same parity as t+1) and V half t+1 (parity of t-1).
-  // Every step issues eight DMA loads, so at the start of a step the loads
-  // of the step before last, which it reads, are done after vmcnt(8).
+  // reads K half t+1 and V half t-1, then refills the buffers it read: K
+  // half t+3 (same parity as t+1) and V half t+1 (parity of t-1). Every step
+  // issues eight DMA loads, so at the start of a step the loads of the step
+  // before last, which it reads, are done after vmcnt(8).
   f32x16 s_cur[2];
   bf16x8 p_prev[2][2];
 #pragma unroll
@@ -553,8 +644,8 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
     load_half(false, j0, 0, kbuf0, dma_off);
     __builtin_amdgcn_s_waitcnt(kWaitVm0);
     bf16x8 kA[4];
-    read_k(kbuf0, kA);
-    mfma_s(kA, s_cur);
+    wk.read_k(kbuf0, kA);
+    wk.mfma_s(kA, s_cur);
     __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
     load_half(false, j0, 1, kbuf1, dma_off);   // K half 1 (tile 0)
     load_half(true, j0, 1, vbuf1, dma_off);   // V of half -1: any tile (its P is 0)
@@ -562,9 +653,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
     load_half(true, j0, 0, vbuf0, dma_off);   // V half 0 (tile 0)
   }
 
-  // One step with the matrix-core and VALU work of the same step in one
-  // scheduling region. kNext: there is a half t+1; kMask: half t may be the
-  // partial last block.
+  // kNext: there is a half t+1; kMask: half t may be the partial last block
   auto step = [&](auto h_c, auto next_c, auto mask_c, int jcur, int jkn, int jvn) {
     constexpr int h = decltype(h_c)::value;
     constexpr bool kNext = decltype(next_c)::value;
@@ -572,46 +661,16 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
     lds_char* const kb = h == 0 ? kbuf1 : kbuf0;  // K half t+1
     lds_char* const vb = h == 0 ? vbuf1 : vbuf0;  // V half t-1
     __builtin_amdgcn_s_waitcnt(kWaitVm8);
-    bf16x8 kA[4];
-    bf16x8 vA[2][2];
-    if constexpr (kNext) read_k(kb, kA);
-    read_v(vb, vA);
-    f32x16 s_next[2];
-    if constexpr (kNext) mfma_s(kA, s_next);
-    mfma_pv(vA, p_prev);
     int valid = 32;
     if constexpr (kMask) {
       if (tail && jcur == last_block) valid = valid_last - 32 * h;
     }
-    bf16x8 p_new[2][2];
-    mask_keys(s_cur, valid);
-    float rs[2];
-    probs(s_cur, p_new, rs);
-    // schedule of this region: the 12 LDS operand reads first (mask 0x100),
-    // ten softmax VALU ops (0x002) while they land, then each of the 16
-    // MFMAs (0x008) followed by four VALU ops, so the matrix cores and the
-    // VALU work on independent data side by side
-    __builtin_amdgcn_sched_group_barrier(0x100, 12, 0);
-    __builtin_amdgcn_sched_group_barrier(0x002, 10, 0);
-#pragma unroll
-    for (int g = 0; g < 16; ++g) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
-    }
-    fixup(s_cur, p_new, rs);
+    wk.template step<kNext>(kb, vb, valid, s_cur, p_prev);
     // refill the two buffers this step read
     __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
     if constexpr (kNext) {
       load_half(false, jkn, h ^ 1, kb, dma_off);
       load_half(true, jvn, h ^ 1, vb, dma_off);
-    }
-#pragma unroll
-    for (int u = 0; u < 2; ++u)
-#pragma unroll
-      for (int tq = 0; tq < 2; ++tq) p_prev[u][tq] = p_new[u][tq];
-    if constexpr (kNext) {
-      s_cur[0] = s_next[0];
-      s_cur[1] = s_next[1];
     }
   };
 
@@ -630,34 +689,202 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
   }
   // last tile: its halves may hold the partial last block
   step(H0{}, T{}, T{}, j0, j1, j0);
-  {
-    // final step: no half t+1; O += V^T P^T of half t-1, softmax of half t,
-    // then the P V of half t itself
-    __builtin_amdgcn_s_waitcnt(kWaitVm0);
-    bf16x8 vA[2][2];
-    read_v(vbuf0, vA);
-    mfma_pv(vA, p_prev);
-    int valid = 32;
-    if (tail && j0 == last_block) valid = valid_last - 32;
-    bf16x8 p_new[2][2];
-    softmax(s_cur, valid, p_new);
-    read_v(vbuf1, vA);
-    mfma_pv(vA, p_new);
-  }
+  __builtin_amdgcn_s_waitcnt(kWaitVm0);
+  wk.last_step(vbuf0, vbuf1, tail && j0 == last_block ? valid_last - 32 : 32, s_cur, p_prev);
 
   float lt[2];
-#pragma unroll
-  for (int tq = 0; tq < 2; ++tq) lt[tq] = pair_sum(l[tq]);
+  wk.row_sums(lt);
   if constexpr (kMode == kLists) {
     if (w.chunk >= 0) {  // a split item: the merge combines the ranges
-      store_partials(o, m, lt, a, w.item, false, lane);
+      store_partials(wk.o, wk.m, lt, a, w.item, false, lane);
       return;
     }
   }
   const float inv[2] = {1.0f / lt[0], 1.0f / lt[1]};
-  const float lse_val[2] = {(m[0] + __log2f(lt[0])) * kLn2, (m[1] + __log2f(lt[1])) * kLn2};
-  write_out_tile(o, inv, lse_val, kbuf0, kbuf1, ro, lse ? lse + (int64_t)w.h * a.n : nullptr, w.i,
+  const float lse_val[2] = {(wk.m[0] + __log2f(lt[0])) * kLn2, (wk.m[1] + __log2f(lt[1])) * kLn2};
+  write_out_tile(wk.o, inv, lse_val, kbuf0, kbuf1, ro, lse ? lse + (int64_t)w.h * a.n : nullptr, w.i,
                  a.n, lane);
+}
+
+// ---- every head dense: kDenseWaves waves per workgroup sharing the K / V tiles
+//
+// A workgroup takes kDenseWaves neighbouring query blocks of one head, and
+// since every one of them walks every key block in order, each K and V half
+// tile is staged in LDS once for all of them. Wave w owns query block
+// kDenseWaves * group + w; a block past the head's last one runs the last
+// block again and stores nothing, so every wave meets every barrier. The K and
+// V half tiles go into a ring of four LDS buffers per tensor (K half x in
+// kring[x % 4], V half x in vring[x % 4]). Step t reads K half t+1 and V half
+// t-1; right after the step's barrier the waves refill the buffers step t-1
+// read (K half t+4, V half t+2), each wave issuing its share of the eight 1 KB
+// DMA instructions, three steps before those buffers are read. Before the
+// barrier each wave waits for its own loads of three steps back, so after it
+// every wave's loads for the step have landed, and every wave has finished
+// the reads of step t-1.
+constexpr int kDenseWaves = 4;
+
+// Group g (rows 8g .. 8g+7) of the 32-row half h of block j into buf: one 1 KB
+// DMA instruction. The descriptor starts at the group and extends over what
+// is left of the head, so rows past the head, and any j outside [0, nb),
+// read zeros.
+__device__ inline void dma_group(const uint16_t* head, uint32_t head_bytes, int nb, int j, int h,
+                                 int g, lds_char* buf, int lane_off) {
+  const uint32_t t = __builtin_amdgcn_readfirstlane(
+      (uint32_t)j < (uint32_t)nb ? ((uint32_t)j * kBlock + 32u * h + 8u * g) * (kHeadDim * 2)
+                                 : head_bytes);
+  const uint32_t rem = __builtin_amdgcn_readfirstlane(t < head_bytes ? head_bytes - t : 0u);
+  const __amdgpu_buffer_rsrc_t r = make_rsrc(reinterpret_cast<const char*>(head) + t, rem);
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)(buf + 1024 * g), 16, lane_off, 0, 0, 0);
+}
+
+__global__ __launch_bounds__(64 * kDenseWaves) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_bf16_dense_kernel(
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
+    uint16_t* __restrict__ out, float* __restrict__ lse, AttnArgs a) {
+  __shared__ __attribute__((aligned(1024))) char kr0[32 * 128];
+  __shared__ __attribute__((aligned(1024))) char kr1[32 * 128];
+  __shared__ __attribute__((aligned(1024))) char kr2[32 * 128];
+  __shared__ __attribute__((aligned(1024))) char kr3[32 * 128];
+  __shared__ __attribute__((aligned(1024))) char vr0[32 * 128];
+  __shared__ __attribute__((aligned(1024))) char vr1[32 * 128];
+  __shared__ __attribute__((aligned(1024))) char vr2[32 * 128];
+  __shared__ __attribute__((aligned(1024))) char vr3[32 * 128];
+  lds_char* const kring[4] = {(lds_char*)kr0, (lds_char*)kr1, (lds_char*)kr2, (lds_char*)kr3};
+  lds_char* const vring[4] = {(lds_char*)vr0, (lds_char*)vr1, (lds_char*)vr2, (lds_char*)vr3};
+  constexpr int kW = kDenseWaves;
+
+  // workgroup b runs on XCD b % 8; each XCD takes a contiguous run of the
+  // (head, group) units, so the workgroups it runs at once walk one head
+  const int nb = a.nb;
+  const int groups = (nb + kW - 1) / kW;
+  const int total = a.heads * groups;
+  const int per_xcd = (total + 7) / 8;
+  const int unit = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
+  if (unit >= total) return;  // the whole workgroup
+  const int hpos = unit / groups;
+  const int hidx = a.order[hpos];
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  const int l32 = lane & 31;
+  const int hf = lane >> 5;
+  const int i_own = (unit - hpos * groups) * kW + wave;
+  const bool valid_block = i_own < nb;
+
+  const int64_t head_off = (int64_t)hidx * a.n * kHeadDim;
+  const uint32_t head_bytes = (uint32_t)(a.n * kHeadDim * 2);
+  const uint16_t* const kh = k + head_off;
+  const uint16_t* const vh = v + head_off;
+
+  Bf16Walk<true> wk;
+  wk.init(make_rsrc(q + head_off, head_bytes), valid_block ? i_own : nb - 1, lane, a.scale_log2);
+
+  // this wave's share of a step's eight DMA instructions n = wave, wave + kW,
+  // ... (n < 4: K group n, else V group n - 4); its group is wave % 4 either way
+  const DmaLaneOffsets dma_off = dma_lane_offset(lane);
+  const int dma_g = wave & 3;
+  const int dma_lane = (dma_g & 1) ? dma_off.odd : dma_off.even;
+  auto issue = [&](int jk, int hk, lds_char* kb, int jv, int hv, lds_char* vb) {
+#pragma unroll
+    for (int n0 = 0; n0 < 8; n0 += kW) {
+      if (n0 + wave < 4) dma_group(kh, head_bytes, nb, jk, hk, dma_g, kb, dma_lane);
+      else dma_group(vh, head_bytes, nb, jv, hv, dma_g, vb, dma_lane);
+    }
+  };
+  // this wave's loads up to `pending` instructions back have landed and its
+  // LDS reads are done; then the workgroup meets (the asm's memory clobber
+  // keeps LDS accesses on their side of the barrier)
+  auto sync = [&](auto pending_c) {
+    constexpr int pending = decltype(pending_c)::value;
+    __builtin_amdgcn_s_waitcnt((0x0F70 | pending) & kWaitLgkm0);
+    asm volatile("s_barrier" ::: "memory");
+  };
+  constexpr int kPending = 2 * (8 / kW);  // two steps of this wave's loads
+
+  const bool tail = (a.n % kBlock) != 0;
+  const int valid_last = (int)(a.n - (int64_t)(nb - 1) * kBlock);
+
+  f32x16 s_cur[2];
+  bf16x8 p_prev[2][2];
+#pragma unroll
+  for (int u = 0; u < 2; ++u)
+#pragma unroll
+    for (int tq = 0; tq < 2; ++tq) p_prev[u][tq] = bf16x8{};  // P of half -1: nothing
+
+  // prologue: K halves 0-3 into kring[0..3]; V half -1 (any data, its P is 0:
+  // V half 1) into vring[3], V halves 0 and 1 into vring[0] and vring[1]
+  issue(0, 0, kring[0], 0, 1, vring[3]);
+  issue(0, 1, kring[1], 0, 0, vring[0]);
+  issue(1, 0, kring[2], 0, 1, vring[1]);
+  issue(1, 1, kring[3], 0, 1, vring[1]);
+  sync(std::integral_constant<int, 0>{});
+  {
+    bf16x8 kA[4];
+    wk.read_k(kring[0], kA);
+    wk.mfma_s(kA, s_cur);
+  }
+
+  // step t = 2j + h with P = t % 4 (the ring slots are then fixed)
+  auto step = [&](auto p_c, auto mask_c, int j) {
+    constexpr int P = decltype(p_c)::value;
+    constexpr int h = P & 1;
+    constexpr bool kMask = decltype(mask_c)::value;
+    sync(std::integral_constant<int, kPending>{});
+    // refill what step t-1 read: K half t+4 (block j+2, half h), V half t+2 (block j+1, half h)
+    issue(j + 2, h, kring[P], j + 1, h, vring[(P + 2) & 3]);
+    const int valid = kMask && tail ? valid_last - 32 * h : 32;
+    wk.template step<true>(kring[(P + 1) & 3], vring[(P + 3) & 3], valid, s_cur, p_prev);
+  };
+  // the last step t = 2nb - 1, P = t % 4
+  auto last = [&](auto p_c) {
+    constexpr int P = decltype(p_c)::value;
+    sync(std::integral_constant<int, 0>{});
+    wk.last_step(vring[(P + 3) & 3], vring[P], tail ? valid_last - 32 : 32, s_cur, p_prev);
+  };
+
+  using F = std::false_type;
+  using T = std::true_type;
+  using P0 = std::integral_constant<int, 0>;
+  using P1 = std::integral_constant<int, 1>;
+  using P2 = std::integral_constant<int, 2>;
+  using P3 = std::integral_constant<int, 3>;
+  int it = 0;  // tiles it and it + 1 per iteration, it even
+  for (; it + 2 < nb; it += 2) {
+    step(P0{}, F{}, it);
+    step(P1{}, F{}, it);
+    step(P2{}, F{}, it + 1);
+    step(P3{}, F{}, it + 1);
+  }
+  if (nb - it == 2) {
+    step(P0{}, F{}, it);
+    step(P1{}, F{}, it);
+    step(P2{}, T{}, it + 1);
+    last(P3{});
+  } else {
+    step(P0{}, T{}, it);
+    last(P1{});
+  }
+
+  if (!valid_block) return;
+  float lt[2];
+  wk.row_sums(lt);
+  const __amdgpu_buffer_rsrc_t ro = make_rsrc(out + head_off, head_bytes);
+  float* const lse_row = lse ? lse + (int64_t)hidx * a.n : nullptr;
+  // straight from the registers: 8-byte stores, once per walk of nb blocks
+#pragma unroll
+  for (int tq = 0; tq < 2; ++tq) {
+    const int query = i_own * kBlock + 32 * tq + l32;
+    const float inv = 1.0f / lt[tq];
+#pragma unroll
+    for (int c = 0; c < 2; ++c)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        bf16x4 ov;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) ov[r] = (__bf16)(wk.o[c][tq][4 * g + r] * inv);
+        __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(i32x2, ov), ro,
+                                              (int)((query * kHeadDim + 32 * c + 8 * g + 4 * hf) * 2), 0, 0);
+      }
+    if (lse_row && hf == 0 && query < a.n) lse_row[query] = (wk.m[tq] + __log2f(lt[tq])) * kLn2;
+  }
 }
 
 // Combines the key ranges of split heads: per query, M = max of the ranges'
@@ -921,8 +1148,15 @@ hipError_t launch_attention(int dtype, const void* q, const void* k, const void*
   if (groups == 0) return hipSuccess;
   const dim3 grid((unsigned)groups);
   if (dtype == 1) {
-    auto kern = a.mode == kStrided ? attn_bf16_kernel<kStrided>
-                : a.mode == kAllDense ? attn_bf16_kernel<kAllDense> : attn_bf16_kernel<kLists>;
+    if (a.mode == kAllDense) {
+      const int64_t units = (int64_t)a.heads * ((a.nb + kDenseWaves - 1) / kDenseWaves);
+      hipLaunchKernelGGL(attn_bf16_dense_kernel, dim3((unsigned)(8 * ((units + 7) / 8))),
+                         dim3(64 * kDenseWaves), 0, s, static_cast<const uint16_t*>(q),
+                         static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v),
+                         static_cast<uint16_t*>(out), lse, a);
+      return hipGetLastError();
+    }
+    auto kern = a.mode == kStrided ? attn_bf16_kernel<kStrided> : attn_bf16_kernel<kLists>;
     hipLaunchKernelGGL(kern, grid, dim3(64), 0, s, static_cast<const uint16_t*>(q),
                        static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v), idx, cnt,
                        static_cast<uint16_t*>(out), lse, a);

@@ -474,19 +474,31 @@ def test_exact_ties_go_to_the_lower_block(gpu_lib):
             np.testing.assert_array_equal(PT.gpu_list(res, 0, i), ref["lists"][0][i])
 
 
-def test_all_dense_table_is_the_dense_baseline(gpu_lib):
+# All-dense layers run the shared-tile kernel (four query blocks of a head per
+# workgroup): one, two and three key blocks, partial last blocks, head counts
+# whose last workgroup has blocks past the head's end, and layers of more than
+# 64 blocks (checked on sampled query blocks).
+@pytest.mark.parametrize("frames,tpf,heads", [(2, 700, 4), (1, 20, 3), (1, 100, 5), (1, 130, 1),
+                                              (1, 1990, 9), (1, 4100, 16), (2, 2200, 16)])
+def test_all_dense_table_is_the_dense_baseline(gpu_lib, frames, tpf, heads):
     import paper_2607_03612_amd as P
 
-    w = Workload("dense", 2, 700, "bf16", ("fixed", 4, 0, 0), heads=4)
+    w = Workload("dense", frames, tpf, "bf16", ("fixed", heads, 0, 0), heads=heads)
+    print(f"all-dense S={frames} T={tpf} H={heads} nb={w.nb}", flush=True)
     q, k, v = make_qkv(w)
-    table = [(O.DENSE, 0)] * 4
+    table = [(O.DENSE, 0)] * heads
     tq, tk, tv = (PT.to_device(x, "bf16") for x in (q, k, v))
     out, lse = P.sparse_attention(tq, tk, tv, table, w.frames, w.tokens_per_frame, want_lse=True)
     out = PT.out_to_numpy(out)
-    for h in range(4):
-        o_ref, l_ref = O.dense_attention(*(O.to_f64(x[h], "bf16") for x in (q, k, v)))
-        assert PT.max_abs(out[h], o_ref) <= PT.TOL_BF16
-        assert PT.max_abs(lse[h].cpu().numpy().astype(np.float64), l_ref) <= PT.LSE_TOL_BF16
+    lse = lse.cpu().numpy().astype(np.float64)
+    n, nb = w.tokens, w.nb
+    blocks = range(nb) if nb <= 40 else sorted({0, 1, 2, nb // 2, nb - 2, nb - 1})
+    for h in range(heads) if nb <= 40 else (0, heads // 2, heads - 1):
+        qh, kh, vh = (O.to_f64(x[h], "bf16") for x in (q, k, v))
+        rows = np.concatenate([np.arange(i * 64, min(i * 64 + 64, n)) for i in blocks])
+        o_ref, l_ref = O.dense_attention(qh[rows], kh, vh)
+        assert PT.max_abs(out[h][rows], o_ref) <= PT.TOL_BF16, (h,)
+        assert PT.max_abs(lse[h][rows], l_ref) <= PT.LSE_TOL_BF16, (h,)
 
 
 # ------------------------------------------ anchor, stride, global probe

@@ -59,3 +59,34 @@ def test_planted_scalar_offset_is_reported():
            "\tbuffer_store_dwordx4 v[6:9], v18, s[0:3], 0 offen\n"
     got = [(op, soff) for op, soff, _ in _buffer_soffsets(text)]
     assert got == [("buffer_load_dwordx4", "s8"), ("buffer_store_dwordx4", "0")]
+
+
+def _kernel_body(text, substr):
+    names = [m.group(1) for m in re.finditer(r"^(\S+):\s*;\s*@\S+", text, re.M) if substr in m.group(1)]
+    assert len(names) == 1, (substr, names)
+    start = text.index(names[0] + ":")
+    return text[start:text.index(".Lfunc_end", start)]
+
+
+def test_sparse_attention_kernels_use_no_scratch(asm):
+    # the list and strided walks fit in the registers of two waves per SIMD:
+    # no spill stores or reloads anywhere in them
+    for mode in ("ILi0E", "ILi2E"):
+        body = _kernel_body(asm["attn.hip"], "attn_bf16_kernel" + mode)
+        assert "scratch_" not in body, mode
+
+
+def test_dense_kernel_loop_has_one_barrier_per_step_and_no_scratch(asm):
+    # the shared-tile dense walk: its loop (the block that branches back to
+    # the loop header) holds four half-tile steps, each one barrier and two
+    # buffer-to-LDS loads per wave, and no scratch access, whose wait would
+    # also wait for the tile loads in flight
+    body = _kernel_body(asm["attn.hip"], "attn_bf16_dense_kernel")
+    header = re.search(r"^(\.LBB\d+_\d+):\s*;\s*=>This Inner Loop Header", body, re.M).group(1)
+    start = body.index(header + ":")
+    end = body.index(header, start + len(header) + 1)  # the branch back to the header
+    loop = body[start:end]
+    assert loop.count("s_barrier") == 4
+    assert len(re.findall(r"buffer_load_dwordx4 .* lds", loop)) == 8
+    assert "scratch_" not in loop
+    assert len(re.findall(r"v_mfma_f32_32x32x16_bf16", loop)) == 64
