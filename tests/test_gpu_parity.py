@@ -501,6 +501,31 @@ def test_all_dense_table_is_the_dense_baseline(gpu_lib, frames, tpf, heads):
         assert PT.max_abs(lse[h][rows], l_ref) <= PT.LSE_TOL_BF16, (h,)
 
 
+def test_all_dense_launch_over_a_subset_of_heads(gpu_lib):
+    """DENSE heads with SKIP heads between them still make an all-dense launch
+    (the shared-tile kernel over the listed heads only): the dense heads get
+    the same bits as in an all-dense table, the SKIP heads keep their rows."""
+    import torch
+
+    import paper_2607_03612_amd as P
+
+    w = Workload("dense-skip", 2, 700, "bf16", ("fixed", 5, 0, 0), heads=5)
+    q, k, v = make_qkv(w, seed=3)
+    tq, tk, tv = (PT.to_device(x, "bf16") for x in (q, k, v))
+    ref, ref_lse = P.sparse_attention(tq, tk, tv, [(O.DENSE, 0)] * 5, w.frames, w.tokens_per_frame,
+                                      want_lse=True)
+    table = [(O.DENSE, 0), (P.SKIP, 0), (O.DENSE, 0), (P.SKIP, 0), (O.DENSE, 0)]
+    out = torch.full_like(tq, 7.0)
+    _, lse = P.sparse_attention(tq, tk, tv, table, w.frames, w.tokens_per_frame, out=out,
+                                want_lse=True)
+    torch.cuda.synchronize()
+    for h in range(5):
+        if h % 2 == 0:
+            assert torch.equal(out[h], ref[h]) and torch.equal(lse[h], ref_lse[h]), h
+        else:
+            assert bool((out[h] == 7.0).all()), h
+
+
 # ------------------------------------------ anchor, stride, global probe
 
 
