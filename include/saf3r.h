@@ -12,6 +12,8 @@
  *   saf3r_select_blocks     kept key blocks per query block, per head class
  *   saf3r_sparse_attention  softmax attention over the kept blocks only
  *
+ * plus a debug check of the kept-block lists (saf3r_validate_index).
+ *
  * Tensor conventions (all calls):
  *   - Q, K, V, O are device arrays [heads, N, 64], row-major, N = frames *
  *     tokens_per_frame (tokens of frame f are [f*T, (f+1)*T)); element type
@@ -22,17 +24,20 @@
  *     sizes stated, and must not alias another argument.
  *   - Alignment: Q, K, V, O, q_pooled, the NMSE inputs and every workspace
  *     are read or written with 16-byte vector accesses and must be 16-byte
- *     aligned; k_pooled, scores and nmse_out 8-byte; block_idx, block_cnt
- *     and lse 4-byte; cosine features to their element size. A misaligned
+ *     aligned; k_pooled, scores and nmse_out 8-byte; block_idx, block_cnt,
+ *     lse and the list check's workspace 4-byte; cosine features to their
+ *     element size. A misaligned
  *     pointer returns SAF3R_ERR_INVALID_ARGUMENT. The library
  *     allocates nothing and keeps no state between calls; calls on different
  *     streams may run concurrently when their outputs do not overlap.
  *   - `problem` and `table` are host pointers read during the call only.
  *   - `stream` is a hipStream_t (NULL = the default stream). Work is enqueued
- *     asynchronously; the call returns after the launches.
+ *     asynchronously; the call returns after the launches (saf3r_validate_index
+ *     alone waits for its result).
  *   - Every argument is validated on the host before anything is launched; a
- *     call that returns an error has enqueued nothing. SAF3R_ERR_HIP reports
- *     a launch error from the HIP runtime.
+ *     call that returns an error has enqueued nothing (but for
+ *     SAF3R_ERR_CORRUPT_INDEX, the outcome of the list check). SAF3R_ERR_HIP
+ *     reports a launch error from the HIP runtime.
  */
 #ifndef SAF3R_H
 #define SAF3R_H
@@ -49,7 +54,8 @@ typedef enum {
   SAF3R_ERR_UNSUPPORTED = -2,      /* head_dim or block other than 64, sizes beyond the limits */
   SAF3R_ERR_CAPACITY = -3,         /* cap or a workspace smaller than required */
   SAF3R_ERR_HIP = -4,              /* the HIP runtime reported an error on launch */
-  SAF3R_ERR_BAD_TABLE = -5         /* unknown pattern class, or a class parameter out of range */
+  SAF3R_ERR_BAD_TABLE = -5,        /* unknown pattern class, or a class parameter out of range */
+  SAF3R_ERR_CORRUPT_INDEX = -6     /* saf3r_validate_index found a list that breaks its form */
 } saf3r_status;
 
 typedef enum { SAF3R_F32 = 0, SAF3R_BF16 = 1 } saf3r_dtype;
@@ -181,6 +187,28 @@ saf3r_status saf3r_select_blocks(const saf3r_problem* problem, const saf3r_head_
                                  double* scores_or_null, void* workspace_or_null,
                                  int64_t workspace_bytes, void* stream);
 
+/* Checks the kept-block lists (a debug call, not on the hot path). For every
+ * query block i of every FRAME_LOCAL, TOPK, ANCHOR, GLOBAL_PROBE and
+ * COSINE_TOPK head h: 0 <= block_cnt[h][i] <= cap, and equal to param for
+ * TOPK and GLOBAL_PROBE heads (Sec. 4.3 keeps exactly that many); the first
+ * block_cnt[h][i] entries of block_idx[h][i] strictly ascending inside
+ * [0, nb), which rules out repeats; the rest of the row -1. These are the
+ * lists saf3r_select_blocks and saf3r_cosine_select write. DENSE, STRIDE and
+ * SKIP heads are not read. Each row is read within its cap entries, whatever
+ * it holds.
+ *   block_idx, block_cnt  device, as for saf3r_sparse_attention
+ *   cap                   entries per row, >= 1
+ *   workspace             device, 8 bytes, 4-byte aligned, overwritten
+ *   first_bad_or_null     host; on SAF3R_ERR_CORRUPT_INDEX, the lowest
+ *                         failing row as h * nb + i
+ * The call enqueues its check on `stream` and waits for the stream to finish
+ * (it reads the result back).
+ * Returns SAF3R_OK; SAF3R_ERR_CORRUPT_INDEX if a row fails; SAF3R_ERR_HIP;
+ * another error code with nothing enqueued. */
+saf3r_status saf3r_validate_index(const saf3r_problem* problem, const saf3r_head_cfg* table,
+                                  const int32_t* block_idx, const int32_t* block_cnt, int32_t cap,
+                                  int32_t* workspace, int32_t* first_bad_or_null, void* stream);
+
 /* Workspace of saf3r_select_blocks that takes every TOPK head in one batch:
  * (TOPK heads) x nb x 64 x C x 4 bytes, C = ceil(nb / 64) rounded up to a
  * multiple of 4 (198 MB for 10 TOPK heads at nb = 2147); 0 without TOPK
@@ -207,7 +235,8 @@ int64_t saf3r_select_workspace_bytes(const saf3r_problem* problem, const saf3r_h
  *                DENSE and STRIDE heads are not read. A list that is not
  *                ascending, repeats a block or holds indices outside [0, nb)
  *                gives unspecified output values but no access outside the
- *                head's N rows of Q, K, V and O: every K/V tile is read
+ *                head's N rows of Q, K, V and O (saf3r_validate_index
+ *                checks a set of lists beforehand): every K/V tile is read
  *                through a buffer descriptor bounded by the head's extent
  *                (an index outside [0, nb) reads a tile of zeros, and so do
  *                the rows past N of a partial last block).

@@ -30,4 +30,5 @@ from .binding import (  # noqa: F401
     SKIP,
     sparse_attention,
     STRIDE,
+    validate_index,
 )

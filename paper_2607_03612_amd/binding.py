@@ -32,8 +32,11 @@ EXPORTS = (
     "saf3r_nmse_workspace_bytes",
     "saf3r_nmse",
     "saf3r_nmse_noalloc",
+    "saf3r_validate_index",
     "saf3r_status_string",
 )
+
+CORRUPT_INDEX = -6  # saf3r_validate_index: a list breaks its form
 
 
 class Problem(ctypes.Structure):
@@ -81,6 +84,8 @@ def _declare(lib):
     lib.saf3r_nmse.restype = I32
     lib.saf3r_nmse_noalloc.argtypes = [P, V, V, V, V]
     lib.saf3r_nmse_noalloc.restype = I32
+    lib.saf3r_validate_index.argtypes = [P, C, V, V, I32, V, ctypes.POINTER(I32), V]
+    lib.saf3r_validate_index.restype = I32
     lib.saf3r_status_string.argtypes = [I32]
     lib.saf3r_status_string.restype = ctypes.c_char_p
 
@@ -336,6 +341,30 @@ def nmse_noalloc(o_full, o_sparse, frames, tokens_per_frame, out, stream=None):
     _check(_lib().saf3r_nmse_noalloc(ctypes.byref(p), _ptr(o_full), _ptr(o_sparse), _ptr(out),
                                      _stream(stream)), "saf3r_nmse_noalloc")
     return out
+
+
+def validate_index(block_idx, block_cnt, table, frames, tokens_per_frame, workspace=None,
+                   dtype=BF16, stream=None):
+    """Checks the kept-block lists of the listed heads (count, strictly
+    ascending entries in range, -1 padding); waits for the stream. Returns
+    ``None`` when every row passes, else the lowest failing row as
+    ``(head, query_block)``."""
+    import torch
+
+    H, nb, cap = block_idx.shape
+    if block_cnt.shape != (H, nb) or len(table) != H:
+        raise ValueError("block_idx [H, nb, cap], block_cnt [H, nb] and the table must agree")
+    if workspace is None:
+        workspace = torch.empty(2, dtype=torch.int32, device=block_idx.device)
+    p = problem(H, frames, tokens_per_frame, dtype)
+    first = ctypes.c_int32(-1)
+    st = _lib().saf3r_validate_index(ctypes.byref(p), head_table(table), _ptr(block_idx),
+                                     _ptr(block_cnt), ctypes.c_int32(cap), _ptr(workspace),
+                                     ctypes.byref(first), _stream(stream))
+    if st == CORRUPT_INDEX:
+        return divmod(first.value, nb)
+    _check(st, "saf3r_validate_index")
+    return None
 
 
 def run_layer(q, k, v, table, frames, tokens_per_frame, stream=None):

@@ -441,6 +441,37 @@ saf3r_status saf3r_sparse_attention(const saf3r_problem* problem, const saf3r_he
                                             lse_or_null, sa, hs));
 }
 
+saf3r_status saf3r_validate_index(const saf3r_problem* problem, const saf3r_head_cfg* table,
+                                  const int32_t* block_idx, const int32_t* block_cnt, int32_t cap,
+                                  int32_t* workspace, int32_t* first_bad_or_null, void* stream) {
+  Shape s;
+  saf3r_status st = check_problem(problem, &s);
+  if (st != SAF3R_OK) return st;
+  st = check_table(s, table);
+  if (st != SAF3R_OK) return st;
+  if (!block_idx || !block_cnt || !workspace || cap < 1) return SAF3R_ERR_INVALID_ARGUMENT;
+  if (!aligned(block_idx, 4) || !aligned(block_cnt, 4) || !aligned(workspace, 4))
+    return SAF3R_ERR_INVALID_ARGUMENT;
+  saf3r::ValidateArgs a{};
+  a.nb = s.nb;
+  a.cap = cap;
+  for (int h = 0; h < s.heads; ++h) {
+    const int p = table[h].pattern;
+    if (!listed_class(p)) continue;  // DENSE, STRIDE and SKIP heads have no list
+    a.head[a.n_heads] = (int16_t)h;
+    a.expect[a.n_heads] = p == SAF3R_TOPK || p == SAF3R_GLOBAL_PROBE ? table[h].param : -1;
+    ++a.n_heads;
+  }
+  if (a.n_heads == 0) return SAF3R_OK;
+  int32_t result[2] = {0, 0};
+  if (saf3r::run_validate_index(block_idx, block_cnt, workspace, a, result,
+                                static_cast<hipStream_t>(stream)) != hipSuccess)
+    return SAF3R_ERR_HIP;
+  if (result[0] == 0) return SAF3R_OK;
+  if (first_bad_or_null) *first_bad_or_null = result[1];
+  return SAF3R_ERR_CORRUPT_INDEX;
+}
+
 int64_t saf3r_cosine_workspace_bytes(const saf3r_problem* problem, int32_t feat_dim) {
   Shape s;
   const saf3r_status st = check_problem(problem, &s);
@@ -538,6 +569,7 @@ const char* saf3r_status_string(int32_t status) {
     case SAF3R_ERR_CAPACITY: return "index capacity or workspace smaller than required";
     case SAF3R_ERR_HIP: return "HIP runtime error on launch";
     case SAF3R_ERR_BAD_TABLE: return "bad pattern table (class or class parameter)";
+    case SAF3R_ERR_CORRUPT_INDEX: return "corrupt kept-block list (count, order, range or padding)";
     default: return "unknown status";
   }
 }

@@ -131,11 +131,25 @@ struct CosineArgs {
   int16_t head[kMaxHeads];
 };
 
+// List check of the listed heads: one wave per (head, query block).
+struct ValidateArgs {
+  int32_t nb;
+  int32_t cap;
+  int32_t n_heads;
+  int16_t head[kMaxHeads];
+  int32_t expect[kMaxHeads];  // by slot: the exact count a row must hold, or -1 (any)
+};
+
 hipError_t launch_pool(int dtype, const void* q, const void* k, double* qp, double* kp,
                        const PoolArgs& a, hipStream_t s);
 hipError_t launch_select_topk(const double* qp, const double* kpT, int32_t* idx, int32_t* cnt,
                               double* scores, const TopKArgs& a, size_t lds_bytes, hipStream_t s);
 hipError_t launch_select_static(int32_t* idx, int32_t* cnt, const StaticArgs& a, hipStream_t s);
+// The list check on `s`, then its result copied to the host and the stream
+// waited for: out[0] = rows that fail, out[1] = the lowest failing row
+// (h * nb + i). `result` is the caller's 8-byte device workspace.
+hipError_t run_validate_index(const int32_t* idx, const int32_t* cnt, int32_t* result,
+                              const ValidateArgs& a, int32_t out[2], hipStream_t s);
 hipError_t launch_select_global(const double* qp, const double* kpT, int32_t* idx, int32_t* cnt,
                                 double* scores, const GlobalArgs& a, hipStream_t s);
 hipError_t launch_cosine(int dtype, const void* f, double* fb, double* sim, int32_t* idx,

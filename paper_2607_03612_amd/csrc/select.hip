@@ -632,6 +632,45 @@ __global__ __launch_bounds__(kStaticThreads) void select_static_kernel(int32_t* 
   if (lane == 0) cnt[row] = len;
 }
 
+// The list check: result[0] counts failing rows, result[1] keeps the lowest
+// one (INT32_MAX while none fails).
+__global__ __launch_bounds__(64) void validate_init_kernel(int32_t* __restrict__ result) {
+  if (threadIdx.x == 0) {
+    result[0] = 0;
+    result[1] = 0x7fffffff;
+  }
+}
+
+// One wave per (listed head, query block): the row's count lies in [0, cap]
+// (and equals the class's exact count where it has one), its first count
+// entries rise strictly inside [0, nb), and the rest of the row is -1. The
+// wave reads only its own row, whatever the row holds.
+__global__ __launch_bounds__(256) void validate_index_kernel(const int32_t* __restrict__ idx,
+                                                             const int32_t* __restrict__ cnt,
+                                                             int32_t* __restrict__ result,
+                                                             ValidateArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int64_t wave = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (wave >= (int64_t)a.n_heads * a.nb) return;
+  const int slot = (int)(wave / a.nb);
+  const int i = (int)(wave - (int64_t)slot * a.nb);
+  const int64_t row = (int64_t)a.head[slot] * a.nb + i;
+  const int c = cnt[row];
+  bool bad = c < 0 || c > a.cap || (a.expect[slot] >= 0 && c != a.expect[slot]);
+  if (!bad) {  // c is the same in every lane
+    const int32_t* list = idx + row * a.cap;
+    for (int p = lane; p < a.cap; p += 64) {
+      const int v = list[p];
+      if (p < c) bad = bad || v < 0 || v >= a.nb || (p > 0 && list[p - 1] >= v);
+      else bad = bad || v != -1;
+    }
+  }
+  if (__ballot(bad) != 0 && lane == 0) {
+    atomicAdd(&result[0], 1);
+    atomicMin(&result[1], (int32_t)row);
+  }
+}
+
 constexpr int kGlobalThreads = 1024;
 constexpr int kGlobalWaves = kGlobalThreads / 64;
 
@@ -876,6 +915,20 @@ hipError_t launch_select_global(const double* qp, const double* kpT, int32_t* id
   hipLaunchKernelGGL(select_global_broadcast_kernel, dim3((unsigned)((waves + 3) / 4)), dim3(256),
                      0, s, idx, cnt, a);
   return hipGetLastError();
+}
+
+hipError_t run_validate_index(const int32_t* idx, const int32_t* cnt, int32_t* result,
+                              const ValidateArgs& a, int32_t out[2], hipStream_t s) {
+  hipLaunchKernelGGL(validate_init_kernel, dim3(1), dim3(64), 0, s, result);
+  const int64_t waves = (int64_t)a.n_heads * a.nb;
+  if (waves > 0)
+    hipLaunchKernelGGL(validate_index_kernel, dim3((unsigned)((waves + 3) / 4)), dim3(256), 0, s,
+                       idx, cnt, result, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  e = hipMemcpyAsync(out, result, 2 * sizeof(int32_t), hipMemcpyDeviceToHost, s);
+  if (e != hipSuccess) return e;
+  return hipStreamSynchronize(s);
 }
 
 hipError_t launch_select_static(int32_t* idx, int32_t* cnt, const StaticArgs& a, hipStream_t s) {

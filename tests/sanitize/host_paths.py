@@ -68,3 +68,13 @@ def test_all_dense_table_is_one_launch():
     t = B.head_table([(B.DENSE, 0)] * 16)
     assert lib.saf3r_sparse_attention(ctypes.byref(p), t, OK, OK, OK, None, None, 0, OK, None,
                                       None, 0, None) == 0
+
+
+@pytest.mark.parametrize("heads,frames,T,table", TABLES)
+def test_list_check_reaches_a_consistent_launch(heads, frames, T, table):
+    lib = B.load()
+    p = _p(heads, frames, T)
+    t = B.head_table(table)
+    cap = lib.saf3r_index_capacity(ctypes.byref(p), t)
+    first = ctypes.c_int32(-1)
+    assert lib.saf3r_validate_index(ctypes.byref(p), t, OK, OK, cap, OK, ctypes.byref(first), None) == 0

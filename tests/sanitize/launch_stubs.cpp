@@ -119,6 +119,17 @@ hipError_t launch_attention(int dtype, const void* q, const void* k, const void*
   return verdict(ok);
 }
 
+// the check's result as the device would report it for lists that pass
+hipError_t run_validate_index(const int32_t* idx, const int32_t* cnt, int32_t* result,
+                              const ValidateArgs& a, int32_t out[2], hipStream_t) {
+  bool ok = idx && cnt && result && out && a.nb >= 1 && a.nb <= kMaxBlocks && a.cap >= 1 &&
+            a.n_heads >= 1 && heads_ok(a.head, a.n_heads, kMaxHeads);
+  for (int i = 0; ok && i < a.n_heads; ++i) ok = a.expect[i] == -1 || (a.expect[i] >= 1 && a.expect[i] <= a.nb);
+  out[0] = 0;
+  out[1] = 0x7fffffff;
+  return verdict(ok);
+}
+
 hipError_t launch_attention_merge(const float* part_o, const float* part_ml, void* out, float*,
                                   const MergeArgs& a, hipStream_t) {
   return verdict(part_o && part_ml && out && blocks_ok(a.n, a.nb) && a.splits == kSplitChunks &&

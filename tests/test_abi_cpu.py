@@ -168,7 +168,7 @@ def test_attention_workspace_bytes_and_validation(B):
 
 def test_status_strings(B):
     lib = B.load()
-    for s in (0, -1, -2, -3, -4, -5, 42):
+    for s in (0, -1, -2, -3, -4, -5, -6, 42):
         assert lib.saf3r_status_string(s)
     assert lib.saf3r_status_string(-3).decode().startswith("index capacity or workspace")
 
@@ -301,3 +301,31 @@ def test_nmse_noalloc_validates_before_launch(B):
     assert nm(ctypes.byref(p), a8, ok, ok, None) == -1
     assert nm(ctypes.byref(p), ok, a8, ok, None) == -1
     assert nm(ctypes.byref(p), ok, ok, a4, None) == -1
+
+
+def test_validate_index_checks_arguments_before_launch(B):
+    """The list check validates like the other calls before it launches; a
+    table without list heads needs no launch at all."""
+    lib = B.load()
+    p = _p(B, heads=3, frames=8, T=1374)  # nb = 172
+    t = B.head_table([(B.TOPK, 12), (B.FRAME_LOCAL, 0), (B.DENSE, 0)])
+    ok, a2 = ctypes.c_void_p(0x1000), ctypes.c_void_p(0x1002)
+    first = ctypes.c_int32(-7)
+    v = lib.saf3r_validate_index
+    assert v(None, t, ok, ok, 12, ok, ctypes.byref(first), None) == -1
+    assert v(ctypes.byref(p), None, ok, ok, 12, ok, ctypes.byref(first), None) == -1
+    assert v(ctypes.byref(_p(B, heads=3, head_dim=32)), t, ok, ok, 12, ok, None, None) == -2
+    assert v(ctypes.byref(p), B.head_table([(B.TOPK, 173), (B.DENSE, 0), (B.DENSE, 0)]),
+             ok, ok, 12, ok, None, None) == -5
+    assert v(ctypes.byref(p), t, None, ok, 12, ok, None, None) == -1
+    assert v(ctypes.byref(p), t, ok, None, 12, ok, None, None) == -1
+    assert v(ctypes.byref(p), t, ok, ok, 12, None, None, None) == -1
+    assert v(ctypes.byref(p), t, ok, ok, 0, ok, None, None) == -1
+    assert v(ctypes.byref(p), t, a2, ok, 12, ok, None, None) == -1
+    assert v(ctypes.byref(p), t, ok, a2, 12, ok, None, None) == -1
+    assert v(ctypes.byref(p), t, ok, ok, 12, a2, None, None) == -1
+    assert first.value == -7  # untouched by a call that fails validation
+    # DENSE, STRIDE and SKIP heads have no lists: nothing to launch or read
+    none = B.head_table([(B.DENSE, 0), (B.STRIDE, 3), (B.SKIP, 0)])
+    assert v(ctypes.byref(p), none, ok, ok, 1, ok, None, None) == 0
+    assert lib.saf3r_status_string(-6).decode().startswith("corrupt kept-block list")

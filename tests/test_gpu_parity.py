@@ -988,3 +988,70 @@ def test_split_attention_on_cosine_heads(gpu_lib):
             assert PT.max_abs(PT.out_to_numpy(out[h, r.start:r.stop]), ref) <= PT.TOL_BF16, (h, i)
             got_lse = lse[h, r.start:r.stop].cpu().numpy().astype(np.float64)
             assert PT.max_abs(got_lse, ref_lse) <= PT.LSE_TOL_BF16, (h, i)
+
+
+# ------------------------------------------------------------ list check
+
+
+def test_validate_index_passes_library_lists_and_finds_each_corruption(gpu_lib):
+    """saf3r_validate_index: the lists the library writes pass (every class);
+    each kind of corruption planted in one row of a copy is reported at that
+    row, the lowest of two bad rows wins, and rows of DENSE / STRIDE heads are
+    never read."""
+    import torch
+
+    import paper_2607_03612_amd as P
+
+    w = Workload("check", 8, 1374, "bf16", ("fixed", 0, 0, 0))
+    S, T, nb = w.frames, w.tokens_per_frame, w.nb
+    table = _all_classes_table(w)
+    H = len(table)
+    q, k, _ = make_qkv(w, heads=range(H))
+    tq, tk = (PT.to_device(x, "bf16") for x in (q, k))
+    qp, kp = P.estimate_blocks(tq, tk, table, S, T)
+    idx, cnt, _ = P.select_blocks(qp, kp, table, S, T)
+    cap = idx.shape[2]
+    assert P.validate_index(idx, cnt, table, S, T) is None
+
+    topk = next(h for h, (p, _) in enumerate(table) if p == O.TOPK)
+    fl = next(h for h, (p, _) in enumerate(table) if p == O.FRAME_LOCAL)
+    row = 37
+    k_top = table[topk][1]
+    assert k_top < cap  # the Top-K rows carry padding
+
+    def planted(h, i, fn):
+        bi, bc = idx.clone(), cnt.clone()
+        fn(bi[h, i], bc[h])
+        return P.validate_index(bi, bc, table, S, T)
+
+    def swap(r, c):
+        r[[1, 2]] = r[[2, 1]]
+
+    cases = {
+        "unsorted": swap,
+        "repeat": lambda r, c: r.__setitem__(1, r[0]),
+        "negative": lambda r, c: r.__setitem__(0, -2),
+        "past nb": lambda r, c: r.__setitem__(int(c[row]) - 1, nb),
+        "padding": lambda r, c: r.__setitem__(cap - 1, 5),
+        "count above cap": lambda r, c: c.__setitem__(row, cap + 1),
+        "negative count": lambda r, c: c.__setitem__(row, -1),
+    }
+    for name, fn in cases.items():
+        assert planted(topk, row, fn) == (topk, row), name
+        assert planted(fl, row, fn) == (fl, row), name
+    # Top-K keeps exactly k: one entry short is reported even when well formed
+    assert planted(topk, row, lambda r, c: (c.__setitem__(row, k_top - 1),
+                                            r.__setitem__(k_top - 1, -1))) == (topk, row)
+    # two bad rows: the lowest (h * nb + i) is reported
+    bi = idx.clone()
+    bi[fl, 100, 0] = -2
+    bi[topk, 5, 0] = nb + 3
+    assert P.validate_index(bi, cnt, table, S, T) == (min(fl, topk), 100 if fl < topk else 5)
+    # DENSE and STRIDE rows are not read, whatever they hold
+    bi, bc = idx.clone(), cnt.clone()
+    for h, (p, _) in enumerate(table):
+        if p in (O.DENSE, O.STRIDE):
+            bi[h].fill_(-9)
+            bc[h].fill_(-9)
+    assert P.validate_index(bi, bc, table, S, T) is None
+    torch.cuda.synchronize()
