@@ -246,11 +246,21 @@ constexpr int kWaitLgkm0 = 0xC07F; // lgkmcnt(0)
 // but not the scalar offset. So rows past the head's last token (a partial
 // last block) read zeros, and a block index outside [0, nb) reads a tile of
 // zeros instead of memory outside the head.
+// head_bytes - t, or 0 when t is at or past the end, on the scalar unit: as
+// plain C the compiler lowers this saturating subtract of two scalars to a
+// copy, a clamped vector subtract and a readfirstlane, three VALU
+// instructions per tile load in the loop. The borrow of s_sub_u32 sets SCC.
+__device__ inline uint32_t rem_bytes(uint32_t head_bytes, uint32_t t) {
+  uint32_t r;
+  asm("s_sub_u32 %0, %1, %2\n\ts_cselect_b32 %0, 0, %0" : "=&s"(r) : "s"(head_bytes), "s"(t) : "scc");
+  return r;
+}
+
 __device__ inline void dma_half(const uint16_t* head, uint32_t head_bytes, int nb, int j, int h,
                                 lds_char* buf, DmaLaneOffsets off) {
   const uint32_t t = __builtin_amdgcn_readfirstlane(
       (uint32_t)j < (uint32_t)nb ? ((uint32_t)j * kBlock + 32u * h) * (kHeadDim * 2) : head_bytes);
-  const uint32_t rem = __builtin_amdgcn_readfirstlane(t < head_bytes ? head_bytes - t : 0u);
+  const uint32_t rem = rem_bytes(head_bytes, t);
   const __amdgpu_buffer_rsrc_t r = make_rsrc(reinterpret_cast<const char*>(head) + t, rem);
   __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)buf, 16, off.even, 0, 0, 0);
   __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)buf, 16, off.odd, 0, 1024, 0);
@@ -325,7 +335,7 @@ template <bool kPin>
 struct Bf16Walk {
   bf16x8 qB[2][4];  // Q^T as the B operand: qB[tq][s] = Q[64i + 32tq + l32][16s + 8hf + (0..7)]
   f32x16 o[2][2];   // O^T tiles [head-dim half c][query half tq]
-  float m[2];       // running max of the log2-scaled scores
+  float nm[2];      // minus the running max of the log2-scaled scores (the fma's addend)
   float l[2];       // this lane's share of the running row sum
   float sc;
   int l32, hf;
@@ -356,7 +366,7 @@ struct Bf16Walk {
       for (int tq = 0; tq < 2; ++tq)
 #pragma unroll
         for (int e = 0; e < 16; ++e) o[c][tq][e] = 0.f;
-    m[0] = m[1] = kNegInf;
+    nm[0] = nm[1] = -kNegInf;
     l[0] = l[1] = 0.f;
     tr_row = 4 * hf + ((lane & 15) >> 2);
     tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
@@ -424,15 +434,15 @@ struct Bf16Walk {
   __device__ __forceinline__ void probs(const f32x16 (&s)[2], bf16x8 (&p)[2][2], float (&rs)[2]) {
 #pragma unroll
     for (int tq = 0; tq < 2; ++tq) {
-      const float mcur = m[tq];
+      const float nmcur = nm[tq];
       float r = 0.f;
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
         bf16x2 pr[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const f32x2 pf = {fast_exp2(fmaf(s[tq][8 * u + 2 * e], sc, -mcur)),
-                            fast_exp2(fmaf(s[tq][8 * u + 2 * e + 1], sc, -mcur))};
+          const f32x2 pf = {fast_exp2(fmaf(s[tq][8 * u + 2 * e], sc, nmcur)),
+                            fast_exp2(fmaf(s[tq][8 * u + 2 * e + 1], sc, nmcur))};
           pr[e] = __builtin_convertvector(pf, bf16x2);
           r = __builtin_amdgcn_fdot2_f32_bf16(pr[e], kOnes, r, false);
         }
@@ -463,9 +473,10 @@ struct Bf16Walk {
 #pragma unroll
         for (int e = 3; e < 15; e += 2) mx = fmaxf(fmaxf(mx, s[tq][e]), s[tq][e + 1]);
         mx = fmaxf(mx, s[tq][15]);
-        const float mnew = fmaxf(pair_max(mx) * sc, m[tq]);
-        const float alpha = fast_exp2(m[tq] - mnew);
-        m[tq] = mnew;
+        // -max(x, m) = min(-x, -m) and (-m) - (-m') = m' - m, exactly
+        const float nmnew = fminf(-(pair_max(mx) * sc), nm[tq]);
+        const float alpha = fast_exp2(nmnew - nm[tq]);
+        nm[tq] = nmnew;
         l[tq] *= alpha;
 #pragma unroll
         for (int c = 0; c < 2; ++c) o[c][tq] *= alpha;
@@ -528,6 +539,10 @@ struct Bf16Walk {
     fixup(s_cur, p_new, rs);
     read_v(vb_cur, vA);
     mfma_pv(vA, p_new);
+  }
+  __device__ __forceinline__ void running_max(float (&m)[2]) const {
+    m[0] = -nm[0];
+    m[1] = -nm[1];
   }
   // the row sums of the two query halves (the lane pair's shares added)
   __device__ __forceinline__ void row_sums(float (&lt)[2]) const {
@@ -602,7 +617,9 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
   if (count <= 0) {  // an empty list: no keys, zero output, LSE -inf
     if constexpr (kMode == kLists) {
       if (w.chunk >= 0) {  // an empty key range: statistics only, the merge skips it
-        store_partials(wk.o, wk.m, wk.l, a, w.item, true, lane);
+        float m[2];
+        wk.running_max(m);
+        store_partials(wk.o, m, wk.l, a, w.item, true, lane);
         return;
       }
     }
@@ -692,16 +709,17 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
   __builtin_amdgcn_s_waitcnt(kWaitVm0);
   wk.last_step(vbuf0, vbuf1, tail && j0 == last_block ? valid_last - 32 : 32, s_cur, p_prev);
 
-  float lt[2];
+  float lt[2], m[2];
   wk.row_sums(lt);
+  wk.running_max(m);
   if constexpr (kMode == kLists) {
     if (w.chunk >= 0) {  // a split item: the merge combines the ranges
-      store_partials(wk.o, wk.m, lt, a, w.item, false, lane);
+      store_partials(wk.o, m, lt, a, w.item, false, lane);
       return;
     }
   }
   const float inv[2] = {1.0f / lt[0], 1.0f / lt[1]};
-  const float lse_val[2] = {(wk.m[0] + __log2f(lt[0])) * kLn2, (wk.m[1] + __log2f(lt[1])) * kLn2};
+  const float lse_val[2] = {(m[0] + __log2f(lt[0])) * kLn2, (m[1] + __log2f(lt[1])) * kLn2};
   write_out_tile(wk.o, inv, lse_val, kbuf0, kbuf1, ro, lse ? lse + (int64_t)w.h * a.n : nullptr, w.i,
                  a.n, lane);
 }
@@ -732,7 +750,7 @@ __device__ inline void dma_group(const uint16_t* head, uint32_t head_bytes, int 
   const uint32_t t = __builtin_amdgcn_readfirstlane(
       (uint32_t)j < (uint32_t)nb ? ((uint32_t)j * kBlock + 32u * h + 8u * g) * (kHeadDim * 2)
                                  : head_bytes);
-  const uint32_t rem = __builtin_amdgcn_readfirstlane(t < head_bytes ? head_bytes - t : 0u);
+  const uint32_t rem = rem_bytes(head_bytes, t);
   const __amdgpu_buffer_rsrc_t r = make_rsrc(reinterpret_cast<const char*>(head) + t, rem);
   __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)(buf + 1024 * g), 16, lane_off, 0, 0, 0);
 }
@@ -883,7 +901,7 @@ __global__ __launch_bounds__(64 * kDenseWaves) __attribute__((amdgpu_waves_per_e
         __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(i32x2, ov), ro,
                                               (int)((query * kHeadDim + 32 * c + 8 * g + 4 * hf) * 2), 0, 0);
       }
-    if (lse_row && hf == 0 && query < a.n) lse_row[query] = (wk.m[tq] + __log2f(lt[tq])) * kLn2;
+    if (lse_row && hf == 0 && query < a.n) lse_row[query] = (__log2f(lt[tq]) - wk.nm[tq]) * kLn2;
   }
 }
 
