@@ -501,6 +501,24 @@ def test_all_dense_table_is_the_dense_baseline(gpu_lib, frames, tpf, heads):
         assert PT.max_abs(lse[h][rows], l_ref) <= PT.LSE_TOL_BF16, (h,)
 
 
+@pytest.mark.parametrize("frames,tpf,heads", [(1, 130, 2), (2, 700, 4)])
+def test_all_dense_table_fp32(gpu_lib, frames, tpf, heads):
+    """fp32 layers have no shared-tile kernel: an all-dense fp32 table runs the
+    list kernel with every head flagged dense."""
+    import paper_2607_03612_amd as P
+
+    w = Workload("dense-f32", frames, tpf, "f32", ("fixed", heads, 0, 0), heads=heads)
+    q, k, v = make_qkv(w)
+    tq, tk, tv = (PT.to_device(x, "f32") for x in (q, k, v))
+    out, lse = P.sparse_attention(tq, tk, tv, [(O.DENSE, 0)] * heads, frames, tpf, want_lse=True)
+    out = PT.out_to_numpy(out)
+    lse = lse.cpu().numpy().astype(np.float64)
+    for h in range(heads):
+        o_ref, l_ref = O.dense_attention(*(O.to_f64(x[h], "f32") for x in (q, k, v)))
+        assert PT.max_abs(out[h], o_ref) <= PT.TOL_F32, h
+        assert PT.max_abs(lse[h], l_ref) <= PT.LSE_TOL_F32, h
+
+
 def test_all_dense_launch_over_a_subset_of_heads(gpu_lib):
     """DENSE heads with SKIP heads between them still make an all-dense launch
     (the shared-tile kernel over the listed heads only): the dense heads get
