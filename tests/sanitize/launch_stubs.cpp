@@ -28,13 +28,13 @@ bool heads_ok(const int16_t* head, int n, int limit) {
 
 bool blocks_ok(int64_t n, int nb) { return n >= 1 && nb == (int)((n + kBlock - 1) / kBlock); }
 
-hipError_t verdict(bool ok) { return ok ? hipSuccess : hipErrorInvalidValue; }
+hipError_t launch_status(bool ok) { return ok ? hipSuccess : hipErrorInvalidValue; }
 
 }  // namespace
 
 hipError_t launch_pool(int dtype, const void* q, const void* k, double* qp, double* kp,
                        const PoolArgs& a, hipStream_t) {
-  return verdict((dtype == 0 || dtype == 1) && q && k && qp && kp && blocks_ok(a.n, a.nb) &&
+  return launch_status((dtype == 0 || dtype == 1) && q && k && qp && kp && blocks_ok(a.n, a.nb) &&
                  heads_ok(a.head, a.n_heads, kMaxHeads));
 }
 
@@ -45,7 +45,7 @@ hipError_t launch_select_topk(const double* qp, const double* kpT, int32_t* idx,
               a.rows_per_group == 8 || a.rows_per_group == 16);
   ok = ok && lds_bytes == topk_lds_bytes(a.rows_per_group, a.nb) && lds_bytes <= 160 * 1024;
   for (int i = 0; ok && i < a.n_heads; ++i) ok = a.topk[i] >= 1 && a.topk[i] <= a.nb && a.topk[i] <= a.cap;
-  return verdict(ok);
+  return launch_status(ok);
 }
 
 hipError_t launch_select_topk_ws(const double* qp, const double* kpT, uint32_t* keys, int32_t* idx,
@@ -53,7 +53,7 @@ hipError_t launch_select_topk_ws(const double* qp, const double* kpT, uint32_t* 
   bool ok = qp && kpT && keys && idx && cnt && blocks_ok(a.n, a.nb) &&
             heads_ok(a.head, a.n_heads, kMaxHeads) && a.n_heads >= 1;
   for (int i = 0; ok && i < a.n_heads; ++i) ok = a.topk[i] >= 1 && a.topk[i] <= a.nb && a.topk[i] <= a.cap;
-  return verdict(ok);
+  return launch_status(ok);
 }
 
 hipError_t launch_select_static(int32_t* idx, int32_t* cnt, const StaticArgs& a, hipStream_t) {
@@ -62,14 +62,14 @@ hipError_t launch_select_static(int32_t* idx, int32_t* cnt, const StaticArgs& a,
   for (int i = 0; ok && i < a.n_heads; ++i)
     ok = a.pattern[i] == kDense || a.pattern[i] == kFrameLocal || a.pattern[i] == kAnchor ||
          a.pattern[i] == kStride;
-  return verdict(ok);
+  return launch_status(ok);
 }
 
 hipError_t launch_select_global(const double* qp, const double* kpT, int32_t* idx, int32_t* cnt,
                                 double*, const GlobalArgs& a, hipStream_t) {
   bool ok = qp && kpT && idx && cnt && blocks_ok(a.n, a.nb) && heads_ok(a.head, a.n_heads, kMaxHeads);
   for (int i = 0; ok && i < a.n_heads; ++i) ok = a.topk[i] >= 1 && a.topk[i] <= a.nb && a.topk[i] <= a.cap;
-  return verdict(ok);
+  return launch_status(ok);
 }
 
 hipError_t launch_cosine(int dtype, const void* f, double* fb, double* sim, int32_t* idx,
@@ -81,12 +81,12 @@ hipError_t launch_cosine(int dtype, const void* f, double* fb, double* sim, int3
     ok = a.group_start[g + 1] > a.group_start[g] && a.group_k[g] >= 1 &&
          a.group_k[g] <= kMaxCosinePerFrame && (g == 0 || a.group_k[g] > a.group_k[g - 1]);
   ok = ok && heads_ok(a.head, a.group_start[a.n_groups], kMaxHeads);
-  return verdict(ok);
+  return launch_status(ok);
 }
 
 hipError_t launch_nmse(int dtype, const void* ref, const void* test, void* workspace, double* out,
                        int heads, int64_t n, hipStream_t) {
-  return verdict((dtype == 0 || dtype == 1) && ref && test && workspace && out && heads >= 1 &&
+  return launch_status((dtype == 0 || dtype == 1) && ref && test && workspace && out && heads >= 1 &&
                  heads <= kMaxHeads && n >= 1);
 }
 
@@ -116,7 +116,7 @@ hipError_t launch_attention(int dtype, const void* q, const void* k, const void*
   // the partials of split items start after the O accumulators
   if (ok && n_split > 0)
     ok = a.part_ml == a.part_o + (int64_t)n_split * a.splits * a.nb * kBlock * kHeadDim;
-  return verdict(ok);
+  return launch_status(ok);
 }
 
 // the check's result as the device would report it for lists that pass
@@ -127,12 +127,12 @@ hipError_t run_validate_index(const int32_t* idx, const int32_t* cnt, int32_t* r
   for (int i = 0; ok && i < a.n_heads; ++i) ok = a.expect[i] == -1 || (a.expect[i] >= 1 && a.expect[i] <= a.nb);
   out[0] = 0;
   out[1] = 0x7fffffff;
-  return verdict(ok);
+  return launch_status(ok);
 }
 
 hipError_t launch_attention_merge(const float* part_o, const float* part_ml, void* out, float*,
                                   const MergeArgs& a, hipStream_t) {
-  return verdict(part_o && part_ml && out && blocks_ok(a.n, a.nb) && a.splits == kSplitChunks &&
+  return launch_status(part_o && part_ml && out && blocks_ok(a.n, a.nb) && a.splits == kSplitChunks &&
                  (a.dtype == 0 || a.dtype == 1) &&
                  heads_ok(a.head, a.n_split, kMaxHeads) && a.n_split >= 1 &&
                  part_ml == part_o + (int64_t)a.n_split * a.splits * a.nb * kBlock * kHeadDim);
